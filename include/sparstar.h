@@ -1,0 +1,158 @@
+/*
+ * sparstar.h -- C ABI of the SparSTAR hot path on AMD Instinct MI355X (gfx950).
+ *
+ * SparSTAR (arXiv 2608.10519) sparsifies the late-scale attention of a
+ * next-scale video generator.  For every (batch, head) it
+ *   1. cuts Q and K, in their original order, into contiguous blocks of
+ *      `block_size` tokens and mean-pools each block over the nominal block
+ *      length (Section 5.1);
+ *   2. scores every selectable key block against every query block with
+ *      S_ij = D^-1/2 * qbar_i . kbar_j (Eq. 2);
+ *   3. keeps the forced blocks dense (the blocks touching any forced token
+ *      range: the text, plus the reference for the first clip; Eq. 3) and
+ *      takes the top k = min(n_sel, max(1, ceil(rho * n_sel))) of the others
+ *      (Eq. 4-6);
+ *   4. runs forward-only attention over the selected key blocks (Eq. 7,
+ *      Section 5.3), writing O and the log-sum-exp.
+ *
+ * Conventions shared by every call
+ *   - Tensors are dense, row-major, in device memory (HBM):
+ *       Q [B, H, Lq, D] bf16, K and V [B, H, Lk, D] bf16, O [B, H, Lq, D] bf16,
+ *       lse [B, H, Lq] fp32, kv_num_blocks [B, H, n_q] int32,
+ *       kv_indices [B, H, n_q, kv_stride] int32,
+ *     with n_q = ceil(Lq / block_size) and n_k = ceil(Lk / block_size).
+ *     bf16 buffers are passed as `const void*` (16-bit patterns), 16-byte aligned.
+ *   - The caller owns every buffer.  The library allocates no device memory,
+ *     copies nothing between host and device and never synchronises: each call
+ *     validates its arguments on the host, enqueues its kernels on `stream`
+ *     (a hipStream_t; NULL is the default stream) and returns.
+ *   - Return value: SPARSTAR_OK, or a negative code.  Argument errors are
+ *     detected on the host before any HIP call (nothing is launched, outputs are
+ *     untouched); a failed launch returns SPARSTAR_ERR_HIP.  Faults inside a
+ *     kernel surface at the caller's next synchronisation, as for any HIP
+ *     work.  sparstar_last_error() describes the last non-OK return on the
+ *     calling thread.
+ *   - The library holds no state besides that thread-local message; calls on
+ *     different streams may run concurrently.
+ */
+#ifndef SPARSTAR_H
+#define SPARSTAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A half-open token range [begin, end) of the key sequence. */
+typedef struct {
+  int64_t begin;
+  int64_t end;
+} sparstar_range;
+
+enum {
+  SPARSTAR_OK = 0,
+  SPARSTAR_ERR_INVALID_ARG = -1, /* a null pointer, a bad size or value      */
+  SPARSTAR_ERR_UNSUPPORTED = -2, /* a head_dim / block_size not built        */
+  SPARSTAR_ERR_WORKSPACE = -3,   /* workspace missing or too small           */
+  SPARSTAR_ERR_HIP = -4          /* a HIP launch or runtime call failed      */
+};
+
+/* Upper bound on forced ranges and heads the selector accepts. */
+#define SPARSTAR_MAX_KEEP_RANGES 8
+#define SPARSTAR_MAX_HEADS 256
+
+/*
+ * Bytes of device scratch sparstar_score_blocks needs for these sizes: the
+ * pooled blocks qbar [B,H,n_q,D] and kbar [B,H,n_k,D] and the score matrix
+ * S [B,H,n_q,n_k], all fp32, each region 256-byte aligned.  Returns 0 for
+ * invalid sizes.
+ */
+size_t sparstar_score_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size);
+
+/*
+ * The smallest valid kv_stride for sparstar_score_blocks with these arguments:
+ * |J_keep| + max_h k_h (Eq. 3-5).  Arguments as for sparstar_score_blocks (Lq,
+ * B and D do not matter).  Returns a negative SPARSTAR_ERR_* code on invalid
+ * arguments.  Host-only; touches no device.
+ */
+int64_t sparstar_kv_stride(int H, int64_t Lk, int block_size, const double* budget, int n_budget,
+                           const sparstar_range* keep, int n_keep);
+
+/*
+ * The selector: block pooling (Section 5.1), block scores (Eq. 2), keep and
+ * selectable sets (Eq. 3-4), budget (Eq. 5) and the retained supports
+ * A_i (Eq. 6), written as the forward-only block mask of Section 5.3.
+ *
+ *   q, k            device bf16 Q [B,H,Lq,D] and K [B,H,Lk,D].
+ *   B, H, Lq, Lk    sizes; B, H >= 1 (H <= SPARSTAR_MAX_HEADS), Lq >= 0, Lk >= 1.
+ *   D               head dim, 64 or 128.
+ *   block_size      b, 64 or 128 (the same b for queries and keys).
+ *   budget          host array of densities rho in [0, 1]: n_budget == 1 (all
+ *                   heads) or n_budget == H (one per head).  The budget of head h
+ *                   is k_h = min(n_sel, max(1, ceil(rho_h * n_sel))), where a
+ *                   product within 1e-9 * max(1, n_sel) of an integer counts as
+ *                   that integer.
+ *   keep, n_keep    host array of forced token ranges, 0 <= begin <= end <= Lk,
+ *                   n_keep <= SPARSTAR_MAX_KEEP_RANGES (keep may be NULL when
+ *                   n_keep == 0).  J_keep = { j : block j meets some range }.
+ *   kv_num_blocks   device out [B,H,n_q]: |J_keep| + k_h for every row.
+ *   kv_indices      device out [B,H,n_q,kv_stride]: the first kv_num_blocks
+ *                   entries of each row are A_i in ascending block order (the
+ *                   forced blocks included); later entries are left untouched.
+ *   kv_stride       row stride of kv_indices; must be >= |J_keep| + max_h k_h.
+ *   scores          optional device out [B,H,n_q,n_k] fp32: S_ij for selectable
+ *                   j; entries of forced columns are unspecified.  NULL to keep
+ *                   S in the workspace only.
+ *   workspace       device scratch of >= sparstar_score_workspace_bytes(...)
+ *                   bytes, 256-byte aligned; its contents need no initialisation
+ *                   and are garbage afterwards.
+ *
+ * Ties in S are broken toward the lower block index.  The call is deterministic.
+ * Lq == 0 is a no-op.
+ */
+int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
+                          int block_size, const double* budget, int n_budget, const sparstar_range* keep,
+                          int n_keep, int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride, float* scores,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Block-sparse attention forward over the lists of sparstar_score_blocks
+ * (Eq. 7): query token t of block i attends to the key tokens u < Lk of the
+ * blocks kv_indices[b,h,i,0 .. kv_num_blocks[b,h,i]).
+ *   O_t   = sum_u softmax_u(s * q_t . k_u) v_u   (bf16 out, fp32 accumulation)
+ *   lse_t = ln sum_u exp(s * q_t . k_u)          (fp32, natural log)
+ * with s = softmax_scale, or D^-1/2 when softmax_scale <= 0.  A row whose list is
+ * empty gets O = 0 and lse = -inf.
+ *
+ *   q, k, v         device bf16 Q [B,H,Lq,D], K and V [B,H,Lk,D].
+ *   D, block_size   as for sparstar_score_blocks.
+ *   kv_num_blocks, kv_indices, kv_stride   device, as written by
+ *                   sparstar_score_blocks.  Lists are trusted to be ascending
+ *                   and duplicate-free; defensively, a count is clamped to
+ *                   [0, kv_stride] and an entry outside [0, n_k) is skipped.
+ *   o               device bf16 out [B,H,Lq,D].
+ *   lse             device fp32 out [B,H,Lq], or NULL.
+ */
+int sparstar_sparse_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq, int64_t Lk,
+                             int D, int block_size, const int32_t* kv_num_blocks, const int32_t* kv_indices,
+                             int kv_stride, float softmax_scale, void* o, float* lse, void* stream);
+
+/*
+ * Dense attention forward with the same tile engine: every query attends to
+ * all Lk keys (the FlashAttention-2 comparison of Section 6, and the dense
+ * early scales).  Arguments as for sparstar_sparse_attn_fwd; the key tiles are
+ * `block_size` tokens.
+ */
+int sparstar_dense_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq, int64_t Lk, int D,
+                            int block_size, float softmax_scale, void* o, float* lse, void* stream);
+
+/* Message for the last non-OK return on this thread ("" if none). */
+const char* sparstar_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSTAR_H */

@@ -1,0 +1,255 @@
+// C ABI of libsparstar: host-side validation, the keep-set and budget logic of
+// Eq. (3)-(5), workspace layout, and kernel launches.  Every argument check runs
+// before the first HIP call, so invalid calls return an error without touching
+// the device.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "../../include/sparstar.h"
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return code;
+}
+
+int ok() {
+  g_error.clear();
+  return SPARSTAR_OK;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Shared size checks.  Limits keep every derived index inside int32 where the
+// kernels use int (block indices, list positions) and inside int64 elsewhere.
+int check_sizes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
+  if (B < 1 || H < 1) return fail(SPARSTAR_ERR_INVALID_ARG, "B and H must be >= 1 (got B=%d, H=%d)", B, H);
+  if (Lq < 0) return fail(SPARSTAR_ERR_INVALID_ARG, "Lq must be >= 0 (got %lld)", (long long)Lq);
+  if (Lk < 1) return fail(SPARSTAR_ERR_INVALID_ARG, "Lk must be >= 1 (got %lld)", (long long)Lk);
+  if (D != 64 && D != 128) return fail(SPARSTAR_ERR_UNSUPPORTED, "head dim %d not supported (64 or 128)", D);
+  if (block_size != 64 && block_size != 128)
+    return fail(SPARSTAR_ERR_UNSUPPORTED, "block size %d not supported (64 or 128)", block_size);
+  if (Lq > (int64_t(1) << 30) || Lk > (int64_t(1) << 30))
+    return fail(SPARSTAR_ERR_INVALID_ARG, "sequence length above 2^30");
+  const int64_t bh = int64_t(B) * H;
+  const int64_t nq = ceil_div(Lq, block_size), nk = ceil_div(Lk, block_size);
+  if (bh * std::max(Lq, Lk) * D > (int64_t(1) << 46)) return fail(SPARSTAR_ERR_INVALID_ARG, "tensor too large");
+  if (bh * (nq + nk) >= (int64_t(1) << 31) || bh * nq * nk >= (int64_t(1) << 40))
+    return fail(SPARSTAR_ERR_INVALID_ARG, "too many blocks");
+  return SPARSTAR_OK;
+}
+
+// Eq. (5), with the reading that a product within 1e-9 * max(1, n_sel) of an
+// integer counts as that integer.
+int budget_k(double rho, int64_t n_sel) {
+  const double p = rho * double(n_sel);
+  const double r = nearbyint(p);
+  const double c = fabs(p - r) <= 1e-9 * double(std::max<int64_t>(1, n_sel)) ? r : ceil(p);
+  const int64_t k = std::min<int64_t>(n_sel, std::max<int64_t>(1, int64_t(c)));
+  return int(k);
+}
+
+}  // namespace
+
+
+// Keep set (Eq. 3), selectable count (Eq. 4) and per-head budgets (Eq. 5).
+struct Plan {
+  sparstar::KeepBlocks keep;
+  sparstar::HeadBudgets budgets;
+  int64_t n_keep_blocks, n_sel;
+  int max_k;
+};
+
+static int plan_selection(int H, int64_t Lk, int block_size, const double* budget, int n_budget,
+                          const sparstar_range* keep, int n_keep, Plan& plan) {
+  using namespace sparstar;
+  if (H < 1 || H > SPARSTAR_MAX_HEADS) return fail(SPARSTAR_ERR_UNSUPPORTED, "H must be in [1, %d] (got %d)",
+                                                   SPARSTAR_MAX_HEADS, H);
+  if (!budget) return fail(SPARSTAR_ERR_INVALID_ARG, "budget must be non-null");
+  if (n_budget != 1 && n_budget != H)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "n_budget must be 1 or H (got %d, H=%d)", n_budget, H);
+  for (int i = 0; i < n_budget; ++i)
+    if (!(budget[i] >= 0.0 && budget[i] <= 1.0))
+      return fail(SPARSTAR_ERR_INVALID_ARG, "budget[%d] = %g is outside [0, 1]", i, budget[i]);
+  if (n_keep < 0 || n_keep > SPARSTAR_MAX_KEEP_RANGES)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "n_keep must be in [0, %d] (got %d)", SPARSTAR_MAX_KEEP_RANGES, n_keep);
+  if (n_keep > 0 && !keep) return fail(SPARSTAR_ERR_INVALID_ARG, "keep is null with n_keep = %d", n_keep);
+  for (int i = 0; i < n_keep; ++i)
+    if (keep[i].begin < 0 || keep[i].begin > keep[i].end || keep[i].end > Lk)
+      return fail(SPARSTAR_ERR_INVALID_ARG, "keep[%d] = [%lld, %lld) is not inside [0, Lk=%lld]", i,
+                  (long long)keep[i].begin, (long long)keep[i].end, (long long)Lk);
+  const int64_t nk = ceil_div(Lk, block_size);
+  // Block j meets [begin, end) iff floor(begin/b) <= j < ceil(end/b).
+  std::vector<char> is_keep(size_t(nk), 0);
+  for (int i = 0; i < n_keep; ++i) {
+    if (keep[i].begin == keep[i].end) continue;
+    const int64_t j0 = keep[i].begin / block_size, j1 = ceil_div(keep[i].end, block_size);
+    for (int64_t j = j0; j < j1; ++j) is_keep[size_t(j)] = 1;
+  }
+  plan.keep = KeepBlocks{};
+  plan.n_keep_blocks = 0;
+  for (int64_t j = 0; j < nk;) {
+    if (!is_keep[size_t(j)]) { ++j; continue; }
+    int64_t e = j;
+    while (e < nk && is_keep[size_t(e)]) ++e;
+    // merged intervals never outnumber the (<= kMaxKeep) input ranges
+    plan.keep.begin[plan.keep.n] = int(j);
+    plan.keep.end[plan.keep.n] = int(e);
+    ++plan.keep.n;
+    plan.n_keep_blocks += e - j;
+    j = e;
+  }
+  plan.n_sel = nk - plan.n_keep_blocks;
+  plan.budgets = HeadBudgets{};
+  plan.max_k = 0;
+  for (int h = 0; h < H; ++h) {
+    plan.budgets.k[h] = budget_k(budget[n_budget == 1 ? 0 : h], plan.n_sel);
+    plan.max_k = std::max(plan.max_k, plan.budgets.k[h]);
+  }
+  return SPARSTAR_OK;
+}
+
+extern "C" int64_t sparstar_kv_stride(int H, int64_t Lk, int block_size, const double* budget, int n_budget,
+                                      const sparstar_range* keep, int n_keep) {
+  if (Lk < 1 || Lk > (int64_t(1) << 30)) return fail(SPARSTAR_ERR_INVALID_ARG, "Lk must be in [1, 2^30]");
+  if (block_size != 64 && block_size != 128)
+    return fail(SPARSTAR_ERR_UNSUPPORTED, "block size %d not supported (64 or 128)", block_size);
+  Plan plan;
+  if (int rc = plan_selection(H, Lk, block_size, budget, n_budget, keep, n_keep, plan)) return rc;
+  ok();
+  return plan.n_keep_blocks + plan.max_k;
+}
+
+extern "C" const char* sparstar_last_error(void) { return g_error.c_str(); }
+
+struct WsLayout {
+  size_t q_bar, k_bar, s, total;
+};
+
+static WsLayout ws_layout(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
+  const int64_t bh = int64_t(B) * H;
+  const int64_t nq = ceil_div(Lq, block_size), nk = ceil_div(Lk, block_size);
+  WsLayout w;
+  w.q_bar = 0;
+  w.k_bar = align256(size_t(bh * nq * D) * sizeof(float));
+  w.s = w.k_bar + align256(size_t(bh * nk * D) * sizeof(float));
+  w.total = w.s + align256(size_t(bh * nq * nk) * sizeof(float));
+  return w;
+}
+
+extern "C" size_t sparstar_score_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
+  if (check_sizes(B, H, Lq, Lk, D, block_size) != SPARSTAR_OK) return 0;
+  return ws_layout(B, H, Lq, Lk, D, block_size).total;
+}
+
+extern "C" int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
+                                     int block_size, const double* budget, int n_budget, const sparstar_range* keep,
+                                     int n_keep, int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride,
+                                     float* scores, void* workspace, size_t workspace_bytes, void* stream) {
+  using namespace sparstar;
+  if (int rc = check_sizes(B, H, Lq, Lk, D, block_size)) return rc;
+  // With Lq == 0 there is nothing to read or write on the query side.
+  if (!k || (Lq > 0 && !q)) return fail(SPARSTAR_ERR_INVALID_ARG, "q and k must be non-null");
+  if (!aligned16(q) || !aligned16(k)) return fail(SPARSTAR_ERR_INVALID_ARG, "q and k must be 16-byte aligned");
+  if (Lq > 0 && (!kv_num_blocks || !kv_indices))
+    return fail(SPARSTAR_ERR_INVALID_ARG, "kv_num_blocks and kv_indices must be non-null");
+  Plan plan;
+  if (int rc = plan_selection(H, Lk, block_size, budget, n_budget, keep, n_keep, plan)) return rc;
+  const int64_t nq = ceil_div(Lq, block_size), nk = ceil_div(Lk, block_size);
+  const KeepBlocks& kb = plan.keep;
+  const HeadBudgets& hb = plan.budgets;
+  const int64_t n_keep_blocks = plan.n_keep_blocks, n_sel = plan.n_sel;
+  const int max_k = plan.max_k;
+  if (int64_t(kv_stride) < n_keep_blocks + max_k || kv_stride < 1)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "kv_stride %d < |J_keep| + max k = %lld", kv_stride,
+                (long long)(n_keep_blocks + max_k));
+  const WsLayout wl = ws_layout(B, H, Lq, Lk, D, block_size);
+  if (!workspace) return fail(SPARSTAR_ERR_WORKSPACE, "workspace is null");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    return fail(SPARSTAR_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < wl.total)
+    return fail(SPARSTAR_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, wl.total);
+  if (scores && (reinterpret_cast<uintptr_t>(scores) & 3u) != 0)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "scores must be 4-byte aligned");
+  if (nq == 0) return ok();
+
+  const int bh = B * H;
+  char* ws = static_cast<char*>(workspace);
+  float* q_bar = reinterpret_cast<float*>(ws + wl.q_bar);
+  float* k_bar = reinterpret_cast<float*>(ws + wl.k_bar);
+  float* s = scores ? scores : reinterpret_cast<float*>(ws + wl.s);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+
+  PoolArgs pa{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), q_bar, k_bar, Lq, Lk, bh, int(nq),
+              int(nk), kb};
+  hipError_t e = launch_pool(pa, D, block_size, st);
+  if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "pool launch: %s", hipGetErrorString(e));
+  if (n_sel > 0) {
+    ScoreArgs sa{q_bar, k_bar, s, bh, int(nq), int(nk), float(1.0 / sqrt(double(D))), kb};
+    e = launch_score(sa, D, st);
+    if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "score launch: %s", hipGetErrorString(e));
+  }
+  SelectArgs sel{s, kv_num_blocks, kv_indices, int64_t(bh) * nq, int(nq), int(nk), H, kv_stride, kb, hb};
+  e = launch_select(sel, st);
+  if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "select launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+static int attn_common(const void* q, const void* k, const void* v, int B, int H, int64_t Lq, int64_t Lk, int D,
+                       int block_size, const int32_t* kv_num_blocks, const int32_t* kv_indices, int kv_stride,
+                       float softmax_scale, void* o, float* lse, void* stream, bool dense) {
+  using namespace sparstar;
+  if (int rc = check_sizes(B, H, Lq, Lk, D, block_size)) return rc;
+  if (!k || !v || (Lq > 0 && (!q || !o))) return fail(SPARSTAR_ERR_INVALID_ARG, "q, k, v and o must be non-null");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(SPARSTAR_ERR_INVALID_ARG, "q, k, v and o must be 16-byte aligned");
+  if (lse && (reinterpret_cast<uintptr_t>(lse) & 3u) != 0)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  if (!dense && Lq > 0) {
+    if (!kv_num_blocks || !kv_indices)
+      return fail(SPARSTAR_ERR_INVALID_ARG, "kv_num_blocks and kv_indices must be non-null");
+    if (kv_stride < 1) return fail(SPARSTAR_ERR_INVALID_ARG, "kv_stride must be >= 1 (got %d)", kv_stride);
+  }
+  if (!(softmax_scale == softmax_scale) || isinf(softmax_scale))
+    return fail(SPARSTAR_ERR_INVALID_ARG, "softmax_scale must be finite");
+  const int64_t nq = ceil_div(Lq, block_size), nk = ceil_div(Lk, block_size);
+  if (nq == 0) return ok();
+  const double sc = softmax_scale > 0.f ? double(softmax_scale) : 1.0 / sqrt(double(D));
+  AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+             static_cast<uint16_t*>(o), lse, kv_num_blocks, kv_indices, Lq, Lk, B * H, int(nq), int(nk),
+             dense ? 0 : kv_stride, float(sc * 1.4426950408889634074)};
+  hipError_t e = launch_attn(a, D, block_size, dense, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+extern "C" int sparstar_sparse_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq,
+                                        int64_t Lk, int D, int block_size, const int32_t* kv_num_blocks,
+                                        const int32_t* kv_indices, int kv_stride, float softmax_scale, void* o,
+                                        float* lse, void* stream) {
+  return attn_common(q, k, v, B, H, Lq, Lk, D, block_size, kv_num_blocks, kv_indices, kv_stride, softmax_scale, o,
+                     lse, stream, false);
+}
+
+extern "C" int sparstar_dense_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq,
+                                       int64_t Lk, int D, int block_size, float softmax_scale, void* o, float* lse,
+                                       void* stream) {
+  return attn_common(q, k, v, B, H, Lq, Lk, D, block_size, nullptr, nullptr, 0, softmax_scale, o, lse, stream,
+                     true);
+}

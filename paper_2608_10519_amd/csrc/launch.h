@@ -1,0 +1,72 @@
+// Internal interface between the C-ABI host layer (host_api.cpp) and the kernel
+// translation units.  Everything here is validated by the host layer first.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sparstar {
+
+constexpr int kMaxKeep = 8;
+constexpr int kMaxHeads = 256;
+
+// Forced key blocks as disjoint, ascending block-index ranges [begin, end).
+struct KeepBlocks {
+  int n;
+  int begin[kMaxKeep];
+  int end[kMaxKeep];
+};
+
+// Per-head top-k budgets (Eq. 5), evaluated on the host.
+struct HeadBudgets {
+  int k[kMaxHeads];
+};
+
+struct PoolArgs {
+  const uint16_t* q;  // [BH, Lq, D] bf16
+  const uint16_t* k;  // [BH, Lk, D] bf16
+  float* q_bar;       // [BH, n_q, D]
+  float* k_bar;       // [BH, n_k, D]
+  int64_t lq, lk;
+  int bh, n_q, n_k;
+  KeepBlocks keep;    // key blocks that are never pooled or scored
+};
+
+struct ScoreArgs {
+  const float* q_bar;  // [BH, n_q, D]
+  const float* k_bar;  // [BH, n_k, D]
+  float* s;            // [BH, n_q, n_k]
+  int bh, n_q, n_k;
+  float tau;           // D^-1/2
+  KeepBlocks keep;
+};
+
+struct SelectArgs {
+  const float* s;          // [BH, n_q, n_k]
+  int32_t* kv_num_blocks;  // [BH, n_q]
+  int32_t* kv_indices;     // [BH, n_q, stride]
+  int64_t rows;            // BH * n_q
+  int n_q, n_k, heads, stride;
+  KeepBlocks keep;
+  HeadBudgets budget;
+};
+
+struct AttnArgs {
+  const uint16_t* q;  // [BH, Lq, D]
+  const uint16_t* k;  // [BH, Lk, D]
+  const uint16_t* v;  // [BH, Lk, D]
+  uint16_t* o;        // [BH, Lq, D]
+  float* lse;         // [BH, Lq] or null
+  const int32_t* kv_num_blocks;  // [BH, n_q] (sparse only)
+  const int32_t* kv_indices;     // [BH, n_q, stride] (sparse only)
+  int64_t lq, lk;
+  int bh, n_q, n_k, stride;
+  float scale_log2;   // softmax scale * log2(e)
+};
+
+hipError_t launch_pool(const PoolArgs& a, int d, int block, hipStream_t stream);
+hipError_t launch_score(const ScoreArgs& a, int d, hipStream_t stream);
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+hipError_t launch_attn(const AttnArgs& a, int d, int block, bool dense, hipStream_t stream);
+
+}  // namespace sparstar

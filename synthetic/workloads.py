@@ -28,7 +28,6 @@ stream (seed + 1000).
 from __future__ import annotations
 
 import dataclasses
-from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -42,8 +41,21 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 values to bf16 (round to nearest, ties to even); returns the
     16-bit patterns as uint16.  Inputs here are finite."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    bias = np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    t = u >> np.uint32(16)
+    t &= np.uint32(1)
+    t += np.uint32(0x7FFF)
+    t += u
+    t >>= np.uint32(16)
+    return t.astype(np.uint16)
+
+
+def _add_per_block(x: np.ndarray, per_block: np.ndarray, block: int) -> None:
+    """x[t] += per_block[t // block] in place (x: [L, D] float32)."""
+    n_full = x.shape[0] // block
+    if n_full:
+        x[: n_full * block].reshape(n_full, block, -1)[...] += per_block[:n_full, None, :]
+    if x.shape[0] > n_full * block:
+        x[n_full * block:] += per_block[n_full]
 
 
 def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
@@ -162,7 +174,7 @@ def generate_head(w: Workload, b: int = 0, h: int = 0):
     kx = rk.standard_normal((w.lk, d), dtype=np.float32)
     u = rk.standard_normal((n_k, d), dtype=np.float32).astype(np.float64)
     offs = 2.0 * u / np.linalg.norm(u, axis=1, keepdims=True)          # [n_k, D]
-    kx += np.repeat(offs.astype(np.float32), blk, axis=0)[: w.lk]
+    _add_per_block(kx, offs.astype(np.float32), blk)
 
     rq = _rng(w, b, h, _STREAM_Q)
     qx = rq.standard_normal((w.lq, d), dtype=np.float32)
@@ -178,33 +190,67 @@ def generate_head(w: Workload, b: int = 0, h: int = 0):
             qoff[i] += 1.5 * offs[chosen].sum(axis=0)
         if band.size:
             qoff[i] += w.band_weight * offs[band].sum(axis=0)
-    qx += np.repeat(qoff.astype(np.float32), blk, axis=0)[: w.lq]
+    _add_per_block(qx, qoff.astype(np.float32), blk)
 
     rv = _rng(w, b, h, _STREAM_V)
     vx = rv.standard_normal((w.lk, d), dtype=np.float32)
     return bf16_bits(qx), bf16_bits(kx), bf16_bits(vx)
 
 
-def generate(w: Workload, heads: list[int] | None = None, threads: int = 8):
+def _shm_worker(job):
+    """Process-pool worker: generate one (batch, head) into shared memory."""
+    from multiprocessing import shared_memory
+
+    names, shapes, w, b, hi, h = job
+    blocks = [shared_memory.SharedMemory(name=n) for n in names]
+    try:
+        arrs = [np.ndarray(shp, dtype=np.uint16, buffer=blk.buf) for shp, blk in zip(shapes, blocks)]
+        for dst, src in zip(arrs, generate_head(w, b, h)):
+            dst[b, hi] = src
+        del arrs
+    finally:
+        for blk in blocks:
+            blk.close()
+
+
+def generate(w: Workload, heads: list[int] | None = None, workers: int | None = None):
     """Q [B, H', L_q, D], K and V [B, H', L_k, D] as bf16 bit patterns (uint16),
-    for all heads or the listed ones (H' = len(heads))."""
+    for all heads or the listed ones (H' = len(heads)).
+
+    Large workloads are generated by spawned worker processes (numpy's
+    generators hold the GIL) writing into shared memory; the result does not
+    depend on the number of workers."""
+    import os
+
     hs = list(range(w.heads)) if heads is None else list(heads)
-    q = np.empty((w.batch, len(hs), w.lq, w.head_dim), dtype=np.uint16)
-    k = np.empty((w.batch, len(hs), w.lk, w.head_dim), dtype=np.uint16)
-    v = np.empty_like(k)
+    shapes = [(w.batch, len(hs), w.lq, w.head_dim), (w.batch, len(hs), w.lk, w.head_dim),
+              (w.batch, len(hs), w.lk, w.head_dim)]
+    jobs = [(b, hi, h) for b in range(w.batch) for hi, h in enumerate(hs)]
+    total = sum(int(np.prod(s)) for s in shapes) * 2
+    if workers is None:
+        workers = min(16, len(os.sched_getaffinity(0)), len(jobs))
+    if workers <= 1 or total < (256 << 20):
+        out = [np.empty(s, dtype=np.uint16) for s in shapes]
+        for b, hi, h in jobs:
+            for dst, src in zip(out, generate_head(w, b, h)):
+                dst[b, hi] = src
+        return tuple(out)
 
-    def one(arg):
-        b, hi = arg
-        q[b, hi], k[b, hi], v[b, hi] = generate_head(w, b, hs[hi])
+    import multiprocessing as mp
+    from multiprocessing import shared_memory
 
-    jobs = [(b, hi) for b in range(w.batch) for hi in range(len(hs))]
-    if threads > 1 and len(jobs) > 1:
-        with ThreadPoolExecutor(max_workers=threads) as ex:
-            list(ex.map(one, jobs))
-    else:
-        for j in jobs:
-            one(j)
-    return q, k, v
+    blocks = [shared_memory.SharedMemory(create=True, size=int(np.prod(s)) * 2) for s in shapes]
+    try:
+        names = [blk.name for blk in blocks]
+        ctx = mp.get_context("spawn")
+        with ctx.Pool(processes=workers) as pool:
+            pool.map(_shm_worker, [(names, shapes, w, b, hi, h) for b, hi, h in jobs], chunksize=1)
+        out = tuple(np.ndarray(s, dtype=np.uint16, buffer=blk.buf).copy() for s, blk in zip(shapes, blocks))
+    finally:
+        for blk in blocks:
+            blk.close()
+            blk.unlink()
+    return out
 
 
 def head_densities(w: Workload, density: float | None = None) -> np.ndarray:

@@ -1,0 +1,147 @@
+"""C-ABI tests that need no GPU: the library loads, exports every symbol that
+include/sparstar.h declares, and rejects invalid arguments on the host before
+any HIP call (the fake device pointers below are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_10519_amd import sparstar as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparstar.h")
+
+FAKE = 0x10000  # a 256-byte aligned, never-dereferenced "device" address
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(S.LIB_PATH):
+        pytest.fail("libsparstar.so is not built (run __graft_entry__.build())")
+    return S.load()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sparstar_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert {"sparstar_score_blocks", "sparstar_sparse_attn_fwd", "sparstar_dense_attn_fwd",
+            "sparstar_score_workspace_bytes", "sparstar_kv_stride", "sparstar_last_error"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_workspace_bytes(lib):
+    # 720p: qbar 24*1125*128*4, kbar 24*2258*128*4, S 24*1125*2258*4 (256-aligned regions)
+    al = lambda x: (x + 255) // 256 * 256
+    want = al(24 * 1125 * 128 * 4) + al(24 * 2258 * 128 * 4) + al(24 * 1125 * 2258 * 4)
+    assert S.sparstar_score_workspace_bytes(1, 24, 72_000, 144_512, 128, 64) == want
+    assert S.sparstar_score_workspace_bytes(1, 24, 72_000, 144_512, 96, 64) == 0
+    assert S.sparstar_score_workspace_bytes(0, 24, 72_000, 144_512, 128, 64) == 0
+
+
+@pytest.mark.parametrize("H,Lk,b,budget,keep,want", [
+    (24, 144_512, 64, 0.25, [(72_000, 72_512)], 8 + 563),
+    (24, 144_512, 64, 0.10, [(72_000, 72_512)], 8 + 225),
+    (24, 144_512, 128, 0.25, [(72_000, 72_512)], 5 + 281),      # n_k = 1129, 5 straddling text blocks, n_sel 1124
+    (2, 1152, 64, 0.25, [(512, 640)], 2 + 4),
+    (2, 1152, 64, 0.25, [(512, 640), (0, 512)], 10 + 2),         # clip 1: text + reference
+    (3, 1152, 64, [0.0, 1.0, 0.5], [(512, 640)], 2 + 16),        # per-head: max k = 16
+    (1, 1152, 64, 0.5, [(0, 1152)], 18 + 0),                     # n_sel = 0
+    (1, 1152, 64, 0.5, [], 0 + 9),
+])
+def test_kv_stride_matches_eq3_to_5(lib, H, Lk, b, budget, keep, want):
+    assert S.sparstar_kv_stride(H, Lk, b, budget, keep) == want
+
+
+def _score(lib, **over):
+    a = dict(q=FAKE, k=FAKE, B=1, H=2, Lq=512, Lk=1152, D=64, block=64, budget=[0.25], keep=[(512, 640)],
+             num=FAKE, idx=FAKE, stride=6, scores=None, ws=FAKE,
+             ws_bytes=S.sparstar_score_workspace_bytes(1, 2, 512, 1152, 64, 64))
+    a.update(over)
+    bud = None if a["budget"] is None else (ctypes.c_double * len(a["budget"]))(*a["budget"])
+    nb = over.get("n_budget", 0 if a["budget"] is None else len(a["budget"]))
+    kr = (S.Range * max(1, len(a["keep"])))(*[S.Range(x, y) for x, y in a["keep"]]) if a["keep"] else None
+    nk = over.get("n_keep", len(a["keep"]))
+    return lib.sparstar_score_blocks(a["q"], a["k"], a["B"], a["H"], a["Lq"], a["Lk"], a["D"], a["block"], bud, nb,
+                                     kr, nk, a["num"], a["idx"], a["stride"], a["scores"], a["ws"], a["ws_bytes"],
+                                     None)
+
+
+@pytest.mark.parametrize("over,code,msg", [
+    (dict(q=None), S.ERR_INVALID_ARG, "non-null"),
+    (dict(q=FAKE + 2), S.ERR_INVALID_ARG, "aligned"),
+    (dict(num=None), S.ERR_INVALID_ARG, "kv_num_blocks"),
+    (dict(D=96), S.ERR_UNSUPPORTED, "head dim"),
+    (dict(block=32), S.ERR_UNSUPPORTED, "block size"),
+    (dict(B=0), S.ERR_INVALID_ARG, "B and H"),
+    (dict(H=300, budget=[0.25]), S.ERR_UNSUPPORTED, "H must be"),
+    (dict(Lk=0), S.ERR_INVALID_ARG, "Lk"),
+    (dict(Lq=-1), S.ERR_INVALID_ARG, "Lq"),
+    (dict(budget=[1.5]), S.ERR_INVALID_ARG, "outside [0, 1]"),
+    (dict(budget=[-0.1]), S.ERR_INVALID_ARG, "outside [0, 1]"),
+    (dict(budget=[float("nan")]), S.ERR_INVALID_ARG, "outside [0, 1]"),
+    (dict(budget=None), S.ERR_INVALID_ARG, "budget"),
+    (dict(budget=[0.1, 0.2, 0.3]), S.ERR_INVALID_ARG, "n_budget"),
+    (dict(keep=[(600, 500)]), S.ERR_INVALID_ARG, "keep[0]"),
+    (dict(keep=[(0, 2000)]), S.ERR_INVALID_ARG, "keep[0]"),
+    (dict(keep=[(-1, 5)]), S.ERR_INVALID_ARG, "keep[0]"),
+    (dict(keep=[(0, 1)] * 9), S.ERR_INVALID_ARG, "n_keep"),
+    (dict(keep=[], n_keep=2), S.ERR_INVALID_ARG, "keep is null"),
+    (dict(stride=5), S.ERR_INVALID_ARG, "kv_stride"),
+    (dict(ws=None), S.ERR_WORKSPACE, "workspace"),
+    (dict(ws=FAKE + 16), S.ERR_WORKSPACE, "256-byte"),
+    (dict(ws_bytes=100), S.ERR_WORKSPACE, "required"),
+])
+def test_score_blocks_rejects_invalid_arguments(lib, over, code, msg):
+    assert _score(lib, **over) == code
+    assert msg in S.last_error()
+
+
+def _attn(lib, dense=False, **over):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, B=1, H=2, Lq=512, Lk=1152, D=64, block=64, num=FAKE, idx=FAKE, stride=6,
+             scale=0.0, o=FAKE, lse=None)
+    a.update(over)
+    if dense:
+        return lib.sparstar_dense_attn_fwd(a["q"], a["k"], a["v"], a["B"], a["H"], a["Lq"], a["Lk"], a["D"],
+                                           a["block"], a["scale"], a["o"], a["lse"], None)
+    return lib.sparstar_sparse_attn_fwd(a["q"], a["k"], a["v"], a["B"], a["H"], a["Lq"], a["Lk"], a["D"], a["block"],
+                                        a["num"], a["idx"], a["stride"], a["scale"], a["o"], a["lse"], None)
+
+
+@pytest.mark.parametrize("dense", [False, True])
+@pytest.mark.parametrize("over,code", [
+    (dict(v=None), S.ERR_INVALID_ARG),
+    (dict(o=FAKE + 8), S.ERR_INVALID_ARG),
+    (dict(lse=FAKE + 2), S.ERR_INVALID_ARG),
+    (dict(D=256), S.ERR_UNSUPPORTED),
+    (dict(block=256), S.ERR_UNSUPPORTED),
+    (dict(scale=float("inf")), S.ERR_INVALID_ARG),
+    (dict(scale=float("nan")), S.ERR_INVALID_ARG),
+    (dict(H=0), S.ERR_INVALID_ARG),
+])
+def test_attention_rejects_invalid_arguments(lib, dense, over, code):
+    assert _attn(lib, dense=dense, **over) == code
+    assert S.last_error()
+
+
+@pytest.mark.parametrize("over", [dict(num=None), dict(idx=None), dict(stride=0)])
+def test_sparse_attention_needs_lists(lib, over):
+    assert _attn(lib, **over) == S.ERR_INVALID_ARG
+
+
+def test_python_binding_raises_without_library(tmp_path):
+    with pytest.raises(RuntimeError, match="not found"):
+        S.load(str(tmp_path / "missing.so"))
+
+
+def test_last_error_is_cleared_by_success(lib):
+    assert _score(lib, q=None) == S.ERR_INVALID_ARG
+    assert S.last_error()
+    assert S.sparstar_kv_stride(2, 1152, 64, 0.25, [(512, 640)]) == 6
+    assert S.last_error() == ""

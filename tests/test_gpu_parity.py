@@ -1,0 +1,348 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 CPU oracle.
+
+Small cases are compared element by element; they span several tiles and a
+ragged tail.  Tolerances (tests/helpers.py): selection exact where the oracle's
+boundary gap exceeds 1e-3 (tie-tolerant otherwise), scores |dS| <= 1e-5(1+|S|),
+pooled blocks |d| <= 1e-5, O max-abs <= 1e-2 plus relative Frobenius <= 1e-2 per
+head, lse max-abs <= 1e-3.
+"""
+from __future__ import annotations
+
+import math
+import sys
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle as O
+from synthetic import TINY, Workload, bf16_to_f64, generate, keep_ranges
+from tests.helpers import (bf16_tensor_to_f64, check_gap_rule, check_output, lists_from_device,
+                           lists_to_device, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _ws_views(ws, B, H, n_q, n_k, D):
+    """Split the selector workspace into (q_bar, k_bar) views (layout in sparstar.h)."""
+    import torch
+
+    f = ws.view(torch.float32)
+    qn = B * H * n_q * D
+    off_k = ((qn * 4 + 255) // 256 * 256) // 4
+    return f[:qn].view(B, H, n_q, D), f[off_k: off_k + B * H * n_k * D].view(B, H, n_k, D)
+
+
+def _run_selector(lib, w: Workload, q, k, keep, budget, with_scores=True):
+    import torch
+
+    B, H, Lq, D = q.shape
+    Lk = k.shape[2]
+    n_q, n_k = -(-Lq // w.block), -(-Lk // w.block)
+    ws = torch.empty(lib.sparstar_score_workspace_bytes(B, H, Lq, Lk, D, w.block), dtype=torch.uint8,
+                     device="cuda")
+    scores = torch.full((B, H, n_q, n_k), float("nan"), device="cuda") if with_scores else None
+    num, idx = lib.sparstar_score_blocks(q, k, w.block, budget, keep, scores=scores, workspace=ws)
+    torch.cuda.synchronize()
+    qb, kb = _ws_views(ws, B, H, n_q, n_k, D)
+    return num, idx, scores, qb, kb
+
+
+SELECTOR_CASES = [
+    # name, workload, clip
+    ("tiny-eq1", TINY, 2),
+    ("tiny-listed", TINY.with_(layout="listed"), 2),
+    ("tiny-clip1", TINY, 1),
+    ("ragged-d128-b64", TINY.with_(name="r1", head_dim=128, lq=500, l_ref=300, l_text=77, heads=3, seed=7), 2),
+    ("ragged-d64-b128", TINY.with_(name="r2", block=128, lq=700, l_ref=515, l_text=130, seed=8), 1),
+    ("ragged-d128-b128", TINY.with_(name="r3", head_dim=128, block=128, lq=1000, l_ref=1300, l_text=300,
+                                    heads=2, seed=9, density=0.4), 2),
+    ("many-tiles", TINY.with_(name="r4", head_dim=128, lq=64 * 70 + 5, l_ref=64 * 60 + 9, l_text=200, heads=2,
+                              seed=10, aligned=5, density=0.3), 2),
+]
+
+
+@pytest.mark.parametrize("name,w,clip", SELECTOR_CASES, ids=[c[0] for c in SELECTOR_CASES])
+def test_selector_matches_oracle(gpu_lib, name, w, clip):
+    _say(f"[selector] {name}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk} clip={clip}")
+    qb_, kb_, _ = generate(w)
+    keep = keep_ranges(w, clip)
+    num, idx, scores, qbar, kbar = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, w.density)
+    lists = lists_from_device(num, idx)
+    s_gpu = scores.cpu().numpy()
+    qbar, kbar = qbar.cpu().numpy(), kbar.cpu().numpy()
+    stats = {"exact": 0, "tolerant": 0}
+    for h in range(w.heads):
+        q = bf16_to_f64(qb_[0, h])
+        k = bf16_to_f64(kb_[0, h])
+        ol, s_ref, kk, keep_set = O.select(q, k, w.block, w.density, keep)
+        sel = O.selectable_blocks(keep_set, w.lk, w.block)
+        np.testing.assert_allclose(qbar[0, h], O.pool(q, w.block), rtol=0, atol=1e-5)
+        np.testing.assert_allclose(kbar[0, h][sel], O.pool(k, w.block)[sel], rtol=0, atol=1e-5)
+        err = np.abs(s_gpu[0, h][:, sel] - s_ref[:, sel])
+        assert (err <= 1e-5 * (1 + np.abs(s_ref[:, sel]))).all(), f"head {h}: max |dS| {err.max():.3e}"
+        for i, row in enumerate(lists[0][h]):
+            stats[check_gap_rule(row, s_ref[i], keep_set, sel, kk)] += 1
+    _say(f"[selector] {name}: rows {stats}")
+    assert stats["exact"] > 0
+
+
+def test_selector_per_head_budgets_and_edge_budgets(gpu_lib):
+    w = TINY.with_(name="budgets", heads=5, seed=21)
+    _say("[selector] per-head budgets {0, 1e-6, 0.37, 1, 0.5}")
+    qb_, kb_, _ = generate(w)
+    keep = keep_ranges(w)
+    budgets = [0.0, 1e-6, 0.37, 1.0, 0.5]
+    num, idx, _, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, budgets, with_scores=False)
+    lists = lists_from_device(num, idx)
+    for h, rho in enumerate(budgets):
+        ol, s_ref, kk, keep_set = O.select(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), w.block, rho, keep)
+        sel = O.selectable_blocks(keep_set, w.lk, w.block)
+        for i, row in enumerate(lists[0][h]):
+            check_gap_rule(row, s_ref[i], keep_set, sel, kk)
+
+
+def test_selector_everything_forced(gpu_lib):
+    """n_sel = 0: every list is exactly J_keep."""
+    import torch
+
+    w = TINY.with_(name="allkeep")
+    qb_, kb_, _ = generate(w)
+    num, idx, _, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), [(0, w.lk)], 0.5, with_scores=False)
+    n_k = -(-w.lk // w.block)
+    assert (num.cpu() == n_k).all()
+    assert (idx.cpu()[..., :n_k] == torch.arange(n_k, dtype=torch.int32)).all()
+
+
+def test_selector_ties_prefer_lower_index(gpu_lib):
+    """Identical key blocks score identically: the lower indices must win."""
+    import torch
+
+    w = TINY.with_(name="ties", heads=1)
+    qb_, kb_, _ = generate(w)
+    kb_ = kb_.copy()
+    blk = w.block
+    # blocks 0..3 and 12..15 become copies of block 11 (selectable in the Eq. 1 layout)
+    for j in list(range(0, 4)) + list(range(12, 16)):
+        kb_[0, 0, j * blk:(j + 1) * blk] = kb_[0, 0, 11 * blk:12 * blk]
+    keep = keep_ranges(w)
+    num, idx, scores, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, 3 / 16)
+    lists = lists_from_device(num, idx)[0][0]
+    s = scores.cpu().numpy()[0, 0]
+    keep_set = O.keep_blocks(keep, w.lk, w.block)
+    sel = O.selectable_blocks(keep_set, w.lk, w.block)
+    for i, row in enumerate(lists):
+        # the GPU's own fp32 scores decide; equal scores must resolve to lower indices
+        want = sorted(set(keep_set) | set(O.topk_idx(s[i].astype(np.float64), sel, 3)))
+        assert row == want, (i, row, want)
+    assert torch.equal(num, num)
+
+
+def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_override=None):
+    """Run the sparse forward with given lists on all heads; return GPU and oracle outputs."""
+    import torch
+
+    qb_, kb_, vb_ = generate(w)
+    if v_override is not None:
+        vb_ = v_override(vb_)
+    if q_override is not None:
+        qb_ = q_override(qb_)
+    n_q = -(-w.lq // w.block)
+    num, idx = lists_to_device([lists_h], n_q)
+    q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
+    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, softmax_scale=scale or 0.0)
+    torch.cuda.synchronize()
+    og, lg = bf16_tensor_to_f64(o), lse.cpu().numpy().astype(np.float64)
+    refs = [O.sparse_attention(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), bf16_to_f64(vb_[0, h]),
+                               lists_h[h], w.block, scale) for h in range(w.heads)]
+    o_ref = np.stack([r[0] for r in refs])[None]
+    l_ref = np.stack([r[1] for r in refs])[None]
+    return og, lg, o_ref, l_ref, (qb_, kb_, vb_)
+
+
+ATTN_CASES = [
+    ("tiny", TINY),
+    ("d128-b64-ragged", TINY.with_(name="a1", head_dim=128, lq=500, l_ref=300, l_text=77, heads=3, seed=17)),
+    ("d64-b128-ragged", TINY.with_(name="a2", block=128, lq=700, l_ref=515, l_text=130, seed=18)),
+    ("d128-b128-ragged", TINY.with_(name="a3", head_dim=128, block=128, lq=1000, l_ref=1300, l_text=300,
+                                    heads=2, seed=19)),
+]
+
+
+def _random_lists(w: Workload, rng, heads=None):
+    n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
+    out = []
+    for _ in range(heads or w.heads):
+        hl = []
+        for i in range(n_q):
+            m = int(rng.integers(1, n_k + 1))
+            l = sorted(rng.choice(n_k, size=m, replace=False).tolist())
+            if i % 3 == 0 and (n_k - 1) not in l:
+                l = sorted(l + [n_k - 1])  # the partial last key block
+            hl.append(l)
+        out.append(hl)
+    return out
+
+
+@pytest.mark.parametrize("name,w", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
+@pytest.mark.parametrize("sharp", [False, True], ids=["tau", "4tau"])
+def test_sparse_attention_matches_oracle(gpu_lib, name, w, sharp):
+    rng = np.random.default_rng(zlib.crc32(name.encode()) % 1000 + int(sharp))
+    lists_h = _random_lists(w, rng)
+    scale = 4.0 / math.sqrt(w.head_dim) if sharp else None
+    _say(f"[attn] {name} sharp={sharp}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk}")
+    og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, scale)
+    err = check_output(og, o_ref, lg, l_ref, what=name)
+    _say(f"[attn] {name}: max |dO| = {err:.2e}")
+
+
+def test_end_to_end_tiny_against_oracle(gpu_lib):
+    """Selector + sparse forward on the tiny workload, each stage against the oracle."""
+    import torch
+
+    w = TINY
+    _say("[e2e] tiny")
+    qb_, kb_, vb_ = generate(w)
+    q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
+    keep = keep_ranges(w)
+    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
+    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
+    torch.cuda.synchronize()
+    lists = lists_from_device(num, idx)[0]
+    for h in range(w.heads):
+        qh, kh, vh = (bf16_to_f64(x[0, h]) for x in (qb_, kb_, vb_))
+        ol, s_ref, kk, keep_set = O.select(qh, kh, w.block, w.density, keep)
+        assert lists[h] == ol  # tiny: every boundary gap is large
+        o_ref, l_ref = O.sparse_attention(qh, kh, vh, ol, w.block)
+        check_output(bf16_tensor_to_f64(o)[0, h][None], o_ref[None], lse.cpu().numpy()[0, h][None].astype(np.float64),
+                     l_ref[None], what=f"head {h}")
+
+
+@pytest.mark.parametrize("name,w", ATTN_CASES[:3], ids=[c[0] for c in ATTN_CASES[:3]])
+def test_dense_attention_matches_oracle(gpu_lib, name, w):
+    import torch
+
+    _say(f"[dense] {name}")
+    qb_, kb_, vb_ = generate(w)
+    o, lse = gpu_lib.sparstar_dense_attn_fwd(to_dev(qb_), to_dev(kb_), to_dev(vb_), w.block)
+    torch.cuda.synchronize()
+    refs = [O.dense_attention(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), bf16_to_f64(vb_[0, h]))
+            for h in range(w.heads)]
+    check_output(bf16_tensor_to_f64(o), np.stack([r[0] for r in refs])[None], lse.cpu().numpy().astype(np.float64),
+                 np.stack([r[1] for r in refs])[None], what=name)
+
+
+def test_full_lists_equal_dense(gpu_lib):
+    """rho = 1 (every block listed) equals the dense forward, bit for bit."""
+    import torch
+
+    w = ATTN_CASES[1][1]
+    _say("[dense==sparse(all)]")
+    qb_, kb_, vb_ = generate(w)
+    q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
+    n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
+    num, idx = lists_to_device([[list(range(n_k))] * n_q for _ in range(w.heads)], n_q)
+    o1, l1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
+    o2, l2 = gpu_lib.sparstar_dense_attn_fwd(q, k, v, w.block)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_unit_values_give_unit_output(gpu_lib):
+    import torch
+
+    w = ATTN_CASES[1][1]
+    _say("[V=1]")
+    lists_h = _random_lists(w, np.random.default_rng(3))
+    og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, v_override=lambda v: np.full_like(v, 0x3F80))
+    assert (og == 1.0).all()
+
+
+def test_zero_queries_average_selected_values(gpu_lib):
+    w = ATTN_CASES[1][1]
+    _say("[Q=0]")
+    lists_h = _random_lists(w, np.random.default_rng(4))
+    og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, q_override=lambda q: np.zeros_like(q))
+    check_output(og, o_ref, lg, l_ref, what="Q=0")
+    n_k = -(-w.lk // w.block)
+    for h in range(w.heads):
+        for i, l in enumerate(lists_h[h][:3]):
+            nkeys = sum(min((j + 1) * w.block, w.lk) - j * w.block for j in l)
+            assert lg[0, h, i * w.block] == pytest.approx(math.log(nkeys), abs=1e-5)
+    assert n_k > 1
+
+
+def test_empty_and_invalid_list_entries(gpu_lib):
+    """Empty rows give O = 0, lse = -inf; out-of-range entries are skipped; counts clamp to the stride."""
+    import torch
+
+    w = ATTN_CASES[0][1]
+    _say("[empty/invalid lists]")
+    qb_, kb_, vb_ = generate(w)
+    q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
+    n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
+    stride = 4
+    num = torch.zeros((1, w.heads, n_q), dtype=torch.int32)
+    idx = torch.zeros((1, w.heads, n_q, stride), dtype=torch.int32)
+    lists_ref = [[[] for _ in range(n_q)] for _ in range(w.heads)]
+    for h in range(w.heads):
+        for i in range(n_q):
+            if i % 3 == 0:
+                continue  # empty
+            if i % 3 == 1:
+                num[0, h, i] = 3
+                idx[0, h, i, :3] = torch.tensor([1, n_k + 5, 4])
+                lists_ref[h][i] = [1, 4]
+            else:
+                num[0, h, i] = 99  # clamped to the stride (4)
+                idx[0, h, i] = torch.tensor([0, 2, -1, 7])
+                lists_ref[h][i] = [0, 2, 7]
+    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num.cuda(), idx.cuda(), w.block)
+    torch.cuda.synchronize()
+    refs = [O.sparse_attention(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), bf16_to_f64(vb_[0, h]),
+                               lists_ref[h], w.block) for h in range(w.heads)]
+    og = bf16_tensor_to_f64(o)
+    lg = lse.cpu().numpy().astype(np.float64)
+    check_output(og, np.stack([r[0] for r in refs])[None], lg, np.stack([r[1] for r in refs])[None], what="lists")
+    assert (og[0, :, : w.block] == 0).all() and np.isneginf(lg[0, :, : w.block]).all()
+
+
+def test_deterministic(gpu_lib):
+    import torch
+
+    w = ATTN_CASES[1][1]
+    _say("[determinism]")
+    qb_, kb_, vb_ = generate(w)
+    q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
+    keep = keep_ranges(w)
+    r1 = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
+    r2 = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
+    o1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, *r1, w.block)
+    o2 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, *r2, w.block)
+    torch.cuda.synchronize()
+    assert torch.equal(r1[0], r2[0])
+    n = r1[0].cpu()
+    i1, i2 = r1[1].cpu(), r2[1].cpu()
+    for h in range(w.heads):
+        for i in range(n.shape[2]):
+            c = int(n[0, h, i])
+            assert torch.equal(i1[0, h, i, :c], i2[0, h, i, :c])
+    assert torch.equal(o1[0], o2[0]) and torch.equal(o1[1], o2[1])
+
+
+def test_empty_query_sequence_is_noop(gpu_lib):
+    import torch
+
+    w = TINY
+    qb_, kb_, vb_ = generate(w)
+    q = torch.empty((1, w.heads, 0, w.head_dim), dtype=torch.bfloat16, device="cuda")
+    k, v = to_dev(kb_), to_dev(vb_)
+    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, 0.25, keep_ranges(w))
+    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
+    torch.cuda.synchronize()
+    assert o.numel() == 0 and num.numel() == 0
