@@ -246,7 +246,7 @@ def test_full_lists_equal_dense(gpu_lib):
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
     n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
-    num, idx = lists_to_device([[list(range(n_k))] * n_q for _ in range(w.heads)], n_q)
+    num, idx = lists_to_device([[[list(range(n_k))] * n_q for _ in range(w.heads)]], n_q)
     o1, l1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
     o2, l2 = gpu_lib.sparstar_dense_attn_fwd(q, k, v, w.block)
     torch.cuda.synchronize()
