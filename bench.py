@@ -92,18 +92,34 @@ def main() -> int:
     ap.add_argument("--density", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--gen-workers", type=int, default=None,
+                    help="input-generation processes (1 = in-process; use 1 under a profiler)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB -> 1 GiB fp32 copy kernel 3 times (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported (the hot path shards "
               "by head with no exchange, but this build measures one GPU only)", file=sys.stderr)
         return 2
 
+    if args.copy_calibration:
+        import torch
+
+        n = 1 << 28  # 1 GiB of fp32
+        x = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            torch.mul(x, 1.0, out=y)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration": {"read_bytes": 4 * n, "write_bytes": 4 * n, "launches": 3}}))
+        return 0
+
     from synthetic import P720, generate, keep_ranges
 
     w = P720 if args.density is None else P720.with_(density=args.density)
     log(f"generating {w.name}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk} rho={w.density}")
     t0 = time.perf_counter()
-    qb, kb, vb = generate(w)
+    qb, kb, vb = generate(w, workers=args.gen_workers)
     log(f"generated in {time.perf_counter() - t0:.1f} s")
 
     import torch

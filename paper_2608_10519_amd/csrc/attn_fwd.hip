@@ -1,62 +1,93 @@
 // Block-sparse attention forward (Eq. 7, Section 5.3) and its dense variant.
 //
-// One work-group per (batch*head, query block of BLK rows); BLK/32 wavefronts,
-// each owning 32 query rows.  The work-group walks the ascending key-block list
-// of its query block; per key block:
-//   1. the K tile (BLK x D) is staged row-major in LDS and the V tile
-//      transposed (D x BLK), from registers prefetched during the previous
-//      tile's math;
-//   2. S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (fp32 accumulate).  Computing
-//      the transpose leaves each lane holding 16 keys of ONE query column, which
-//      is exactly the B-operand layout P^T needs below, so the softmax state
-//      (running max m and sum l) is lane-local;
-//   3. online softmax in the log2 domain; P is rounded to bf16 once.  Two row
-//      sums are kept: over the rounded values (normalises O, so the weights
-//      applied to V sum to one and V == 1 gives O == 1 exactly) and over the
-//      fp32 values (for the log-sum-exp);
-//   4. O^T += V^T P^T on the same MFMA (O^T accumulators keep a lane's query
-//      column together, so the rescale by exp2(m_old - m_new) is lane-local).
-// The epilogue writes O = O^T / l in bf16 and lse = ln2 * (m + log2 l_fp32).
+// Work decomposition.  One work-group per (batch*head, query block of BLK
+// rows), launched head-major so that all eight XCDs work on the same head at a
+// time and that head's K/V (74 MB at the 720p shape) stays resident in the
+// 256 MB last-level cache.  The work-group has 2 * BLK/32 wavefronts: wave w
+// owns the 32-row query slice (w % (BLK/32)) and the key half (w / (BLK/32)) of
+// every key block, so each wave touches only half of each K and V tile and the
+// work-group keeps two waves per SIMD resident (<= 256 VGPRs each).
 //
-// MFMA layouts used (v_mfma_f32_32x32x16_bf16, lane l, h = l / 32):
+// Per key block of the query block's ascending list:
+//   * the K tile (BLK x D) is stored row-major in LDS (16-byte row padding) and
+//     the V tile transposed (D x BLK) in an XOR-swizzled layout whose 8-byte
+//     chunks are bank-conflict-free both for the transposing writes and for the
+//     MFMA operand reads.  LDS is double-buffered: the tile of step t+1 is written
+//     while step t computes, so there is one barrier per step, and the global
+//     loads of step t+2 are in flight during the whole step;
+//   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (fp32 accumulate).  The
+//     transpose leaves each lane holding 16 keys of ONE query column -- exactly
+//     the B-operand layout P^T needs -- so the softmax state is lane-local up to
+//     one cross-half (lane l <-> l+32) max per step (v_permlane32_swap);
+//   * online softmax in the log2 domain with the scale folded into one FMA,
+//     and lazy rescaling: O and l are only rescaled when a query's running
+//     maximum grows by more than 2^8 (P then stays <= 256, exact enough in fp32
+//     and bf16), which skips nearly all rescales after the first steps;
+//   * O^T += V^T P^T on the same MFMA (P rounded to bf16 once).
+// The two key halves of a query slice each hold a partial (m, l, O); they are
+// merged once through LDS at the end.  O = O^T / l in bf16, lse = ln2*(m + log2 l).
+//
+// MFMA layouts (v_mfma_f32_32x32x16_bf16, lane l, h = l / 32):
 //   A[m][k]: m = l % 32, k = 8h + i (i = 0..7 of the lane's bf16x8)
 //   B[k][n]: n = l % 32, k = 8h + i
-//   C[m][n]: n = l % 32, m = 8 (a / 4) + 4h + (a % 4) for accumulator a = 0..15
-// The contraction only needs A and B to agree on k, so keys may be permuted
-// consistently: the P^T operand reuses the S^T C layout directly and the V^T
-// operand reads the same key permutation from LDS.
+//   C[m][n]: n = l % 32, m = 8 (a / 4) + 4h + (a % 4), accumulator a = 0..15
+// A and B only need to agree on k, so keys may be permuted consistently: the
+// P^T operand reuses the S^T C layout directly, and the V^T operand reads the
+// same key permutation from LDS.
 #include "device_common.h"
 
 namespace sparstar {
 
 template <int D, int BLK>
 struct AttnCfg {
-  static constexpr int NW = BLK / 32;         // wavefronts (32 query rows each)
-  static constexpr int NT = NW * 64;          // threads
-  static constexpr int KLD = D + 8;           // K tile row pitch (bf16), padded
-  static constexpr int VLD = BLK + 8;         // V^T tile row pitch (bf16), padded
-  static constexpr int KCH = BLK * D / 8 / NT;          // 16-byte K chunks per thread
-  static constexpr int VGR = (BLK / 4) * (D / 8) / NT;  // 4-key x 8-d V groups per thread
-  static constexpr int KT = BLK / 32;         // 32-key sub-tiles per key block
+  static constexpr int NQS = BLK / 32;        // 32-row query slices
+  static constexpr int NW = 2 * NQS;          // waves: (query slice, key half)
+  static constexpr int NT = 64 * NW;          // threads
+  static constexpr int KH = BLK / 2;          // keys per key half
+  static constexpr int KT = KH / 32;          // 32-key sub-tiles per wave and step
   static constexpr int DS = D / 16;           // MFMA k-steps over D
   static constexpr int DT = D / 32;           // 32-row d tiles of O^T
+  static constexpr int KLD = D + 8;           // K tile row pitch in bf16 (16-byte pad)
+  static constexpr int K_ELEMS = BLK * KLD;
+  static constexpr int V_ELEMS = D * BLK;     // V^T rows of BLK keys, swizzled, unpadded
+  static constexpr int STAGE = K_ELEMS + V_ELEMS;
+  static constexpr int KCH = BLK * D / 8 / NT;   // 16-byte K chunks per thread
+  static constexpr int VG = BLK * D / 32;        // (4 keys x 8 d) V groups per tile
   static_assert(KCH * NT * 8 == BLK * D, "K tile split");
-  static_assert(VGR * NT * 32 == BLK * D, "V tile split");
+  static_assert(VG <= NT, "one V group per thread at most");
 };
 
-template <int D, int BLK, bool DENSE>
-__global__ __launch_bounds__(BLK * 2) void attn_fwd_kernel(AttnArgs a) {
-  using C = AttnCfg<D, BLK>;
-  __shared__ __attribute__((aligned(16))) uint16_t ks[BLK * C::KLD];
-  __shared__ __attribute__((aligned(16))) uint16_t vt[D * C::VLD];
+// Element offset of V^T[d][key] in the swizzled layout: rows of BLK keys whose
+// 4-key (8-byte) chunks are permuted by f(d) = ((d >> 3) & 15) ^ ((d & 7) << 1).
+template <int BLK>
+__device__ __forceinline__ int vt_off(int d, int key) {
+  const int f = ((d >> 3) & 15) ^ ((d & 7) << 1);
+  return d * BLK + (((key >> 2) ^ f) << 2) + (key & 3);
+}
 
-  const int64_t nwork = (int64_t)a.bh * a.n_q;
-  const int64_t work = xcd_linear(blockIdx.x, nwork);
-  const int64_t bh = work / a.n_q;
-  const int qb = (int)(work % a.n_q);
+__device__ __forceinline__ float half_swap_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float half_swap_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int D, int BLK, bool DENSE>
+__global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_fwd_kernel(AttnArgs a) {
+  using C = AttnCfg<D, BLK>;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+
+  const int64_t bh = blockIdx.x / a.n_q;
+  const int qb = (int)(blockIdx.x % a.n_q);
 
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
   const int l32 = lane % 32, hh = lane / 32;
+  const int qs = wave % C::NQS;   // query slice
+  const int kh = wave / C::NQS;   // key half
 
   const uint16_t* kbase = a.k + bh * a.lk * D;
   const uint16_t* vbase = a.v + bh * a.lk * D;
@@ -72,20 +103,26 @@ __global__ __launch_bounds__(BLK * 2) void attn_fwd_kernel(AttnArgs a) {
     nblk = nblk < 0 ? 0 : (nblk > a.stride ? a.stride : nblk);
     list = a.kv_indices + r * a.stride;
   }
-  auto block_at = [&](int it) -> int {
-    if constexpr (DENSE) return it;
-    int j = __builtin_amdgcn_readfirstlane(list[it]);
-    return (j >= 0 && j < a.n_k) ? j : -1;
+  // first list position >= it holding a valid block; the block (or -1) in blk
+  auto next_valid = [&](int it, int& blk) -> int {
+    blk = -1;
+    for (; it < nblk; ++it) {
+      int j;
+      if constexpr (DENSE) j = it;
+      else j = __builtin_amdgcn_readfirstlane(list[it]);
+      if (j >= 0 && j < a.n_k) { blk = j; break; }
+    }
+    return it;
   };
 
   // ---- Q fragment (B operand of S^T = K Q^T): Q[q][16 s + 8 hh .. +7]
-  const int64_t q_row = (int64_t)qb * BLK + wave * 32 + l32;
+  const int64_t q_row = (int64_t)qb * BLK + qs * 32 + l32;
   const bool q_ok = q_row < a.lq;
-  const uint16_t* qp = a.q + (bh * a.lq + (q_row < a.lq ? q_row : 0)) * D;
+  const uint16_t* qp = a.q + (bh * a.lq + (q_ok ? q_row : 0)) * D;
   bf16x8 qf[C::DS];
 #pragma unroll
   for (int s = 0; s < C::DS; ++s) {
-    uint4 u = q_ok ? *reinterpret_cast<const uint4*>(qp + 16 * s + 8 * hh) : make_uint4(0, 0, 0, 0);
+    const uint4 u = q_ok ? *reinterpret_cast<const uint4*>(qp + 16 * s + 8 * hh) : make_uint4(0, 0, 0, 0);
     qf[s] = __builtin_bit_cast(bf16x8, u);
   }
 
@@ -94,11 +131,12 @@ __global__ __launch_bounds__(BLK * 2) void attn_fwd_kernel(AttnArgs a) {
   for (int t = 0; t < C::DT; ++t)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc_o[t][e] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f, le_run = 0.f;
+  float m_run = -INFINITY;  // running max (log2 domain), shared by both lane halves
+  float l_run = 0.f;        // this lane's partial row sum (its 16 keys per sub-tile)
 
-  // ---- global -> register prefetch of one key block
+  // ---- global -> register prefetch and register -> LDS store of one tile
   uint4 kreg[C::KCH];
-  uint4 vreg[C::VGR][4];
+  uint4 vreg[4];
   auto load_tile = [&](int blk) {
     const int64_t key0 = (int64_t)blk * BLK;
 #pragma unroll
@@ -108,32 +146,30 @@ __global__ __launch_bounds__(BLK * 2) void attn_fwd_kernel(AttnArgs a) {
       const int64_t key = key0 + row;
       kreg[r] = key < a.lk ? *reinterpret_cast<const uint4*>(kbase + key * D + col * 8) : make_uint4(0, 0, 0, 0);
     }
-#pragma unroll
-    for (int r = 0; r < C::VGR; ++r) {
-      const int g = tid + C::NT * r;
-      const int dg = g % (D / 8), kg = g / (D / 8);
+    if (tid < C::VG) {
+      const int dg = tid % (D / 8), kg = tid / (D / 8);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int64_t key = key0 + 4 * kg + e;
-        vreg[r][e] = key < a.lk ? *reinterpret_cast<const uint4*>(vbase + key * D + dg * 8) : make_uint4(0, 0, 0, 0);
+        vreg[e] = key < a.lk ? *reinterpret_cast<const uint4*>(vbase + key * D + dg * 8) : make_uint4(0, 0, 0, 0);
       }
     }
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](int stage) {
+    uint16_t* ks = smem + stage * C::STAGE;
+    uint16_t* vt = ks + C::K_ELEMS;
 #pragma unroll
     for (int r = 0; r < C::KCH; ++r) {
       const int c = tid + C::NT * r;
       const int row = c / (D / 8), col = c % (D / 8);
       *reinterpret_cast<uint4*>(&ks[row * C::KLD + col * 8]) = kreg[r];
     }
-#pragma unroll
-    for (int r = 0; r < C::VGR; ++r) {
-      const int g = tid + C::NT * r;
-      const int dg = g % (D / 8), kg = g / (D / 8);
-      const uint32_t w0[4] = {vreg[r][0].x, vreg[r][0].y, vreg[r][0].z, vreg[r][0].w};
-      const uint32_t w1[4] = {vreg[r][1].x, vreg[r][1].y, vreg[r][1].z, vreg[r][1].w};
-      const uint32_t w2[4] = {vreg[r][2].x, vreg[r][2].y, vreg[r][2].z, vreg[r][2].w};
-      const uint32_t w3[4] = {vreg[r][3].x, vreg[r][3].y, vreg[r][3].z, vreg[r][3].w};
+    if (tid < C::VG) {
+      const int dg = tid % (D / 8), kg = tid / (D / 8);
+      const uint32_t w0[4] = {vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w};
+      const uint32_t w1[4] = {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w};
+      const uint32_t w2[4] = {vreg[2].x, vreg[2].y, vreg[2].z, vreg[2].w};
+      const uint32_t w3[4] = {vreg[3].x, vreg[3].y, vreg[3].z, vreg[3].w};
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
         // d = 8 dg + 2p (low halves) and 8 dg + 2p + 1 (high halves); keys 4 kg .. 4 kg + 3
@@ -142,84 +178,82 @@ __global__ __launch_bounds__(BLK * 2) void attn_fwd_kernel(AttnArgs a) {
         lo.y = (w2[p] & 0xffffu) | (w3[p] << 16);
         hi.x = (w0[p] >> 16) | (w1[p] & 0xffff0000u);
         hi.y = (w2[p] >> 16) | (w3[p] & 0xffff0000u);
-        *reinterpret_cast<uint2*>(&vt[(8 * dg + 2 * p) * C::VLD + 4 * kg]) = lo;
-        *reinterpret_cast<uint2*>(&vt[(8 * dg + 2 * p + 1) * C::VLD + 4 * kg]) = hi;
+        *reinterpret_cast<uint2*>(&vt[vt_off<BLK>(8 * dg + 2 * p, 4 * kg)]) = lo;
+        *reinterpret_cast<uint2*>(&vt[vt_off<BLK>(8 * dg + 2 * p + 1, 4 * kg)]) = hi;
       }
     }
   };
 
-  // find the first valid block
-  int it = 0;
-  int cur = -1;
-  while (it < nblk && (cur = block_at(it)) < 0) ++it;
-  if (cur >= 0) load_tile(cur);
+  int cur, nxt, nn;
+  int it = next_valid(0, cur);
+  int it_n = next_valid(it + 1, nxt);
+  if (cur >= 0) {
+    load_tile(cur);
+    store_tile(0);
+    if (nxt >= 0) load_tile(nxt);
+  }
+  __syncthreads();
 
   const float sl2 = a.scale_log2;
+  int stage = 0;
   while (cur >= 0) {
-    // next valid block
-    int it_next = it + 1, nxt = -1;
-    while (it_next < nblk && (nxt = block_at(it_next)) < 0) ++it_next;
+    const uint16_t* ks = smem + stage * C::STAGE;
+    const uint16_t* vt = ks + C::K_ELEMS;
 
-    __syncthreads();  // previous tile fully consumed
-    store_tile();
-    __syncthreads();
-    if (nxt >= 0) load_tile(nxt);
-
-    // ---- S^T = K Q^T
+    // ---- S^T = K Q^T for this wave's keys
     f32x16 acc_s[C::KT];
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc_s[kt][e] = 0.f;
+      const uint16_t* kr = &ks[(kh * C::KH + kt * 32 + l32) * C::KLD + 8 * hh];
 #pragma unroll
       for (int s = 0; s < C::DS; ++s) {
-        const uint4 u = *reinterpret_cast<const uint4*>(&ks[(kt * 32 + l32) * C::KLD + 16 * s + 8 * hh]);
+        const uint4 u = *reinterpret_cast<const uint4*>(kr + 16 * s);
         acc_s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u), qf[s], acc_s[kt], 0, 0, 0);
       }
     }
 
-    // ---- online softmax (log2 domain); keys >= Lk masked
+    // ---- keys >= Lk (only in a partial last block) are masked
     const int64_t key0 = (int64_t)cur * BLK;
-    const bool partial = key0 + BLK > a.lk;
+    if (key0 + BLK > a.lk) {
+#pragma unroll
+      for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = kh * C::KH + kt * 32 + 8 * (e / 4) + 4 * hh + (e % 4);
+          if (key0 + key >= a.lk) acc_s[kt][e] = -INFINITY;
+        }
+    }
+
+    // ---- online softmax with lazy rescaling
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float z = acc_s[kt][e] * sl2;
-        if (partial) {
-          const int key = kt * 32 + 8 * (e / 4) + 4 * hh + (e % 4);
-          if (key0 + key >= a.lk) z = -INFINITY;
-        }
-        acc_s[kt][e] = z;
-        mx = fmaxf(mx, z);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
-
-    float ls = 0.f, le = 0.f;
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc_s[kt][e]);
+    mx = half_swap_max(mx) * sl2;  // this step's max logit (log2 domain) for the lane's query
+    if (__any(mx > m_run + 8.0f)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc_o[t][e] *= alpha;
+      m_run = m_new;
+    }
+    const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
     uint32_t pk[C::KT][8];  // bf16 pairs of P^T, per 32-key sub-tile
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; e += 2) {
-        const float p0 = exp2f(acc_s[kt][e] - m_use), p1 = exp2f(acc_s[kt][e + 1] - m_use);
-        const uint32_t w = pack_bf16(p0, p1);
-        pk[kt][e / 2] = w;
-        ls += bf16_lo(w) + bf16_hi(w);
-        le += p0 + p1;
+        const float p0 = exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
+        const float p1 = exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
+        pk[kt][e / 2] = pack_bf16(p0, p1);
+        l_run += p0 + p1;
       }
-    ls += __shfl_xor(ls, 32, 64);
-    le += __shfl_xor(le, 32, 64);
-    l_run = l_run * alpha + ls;
-    le_run = le_run * alpha + le;
-    m_run = m_new;
-#pragma unroll
-    for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc_o[t][e] *= alpha;
 
     // ---- O^T += V^T P^T over 16-key k-steps
 #pragma unroll
@@ -227,45 +261,81 @@ __global__ __launch_bounds__(BLK * 2) void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         // accumulators a = 8 half + i of sub-tile kt hold keys
-        //   32 kt + 16 half + 4 hh + i       (i = 0..3)
-        //   32 kt + 16 half + 8 + 4 hh + i-4 (i = 4..7)
+        //   base + 4 hh + i (i = 0..3) and base + 8 + 4 hh + (i - 4) (i = 4..7),
+        // base = kh * KH + 32 kt + 16 half
         uint4 pu;
         pu.x = pk[kt][4 * half + 0];
         pu.y = pk[kt][4 * half + 1];
         pu.z = pk[kt][4 * half + 2];
         pu.w = pk[kt][4 * half + 3];
         const bf16x8 pb = __builtin_bit_cast(bf16x8, pu);
-        const int kcol = 32 * kt + 16 * half + 4 * hh;
+        const int kc = kh * C::KH + 32 * kt + 16 * half + 4 * hh;
 #pragma unroll
         for (int t = 0; t < C::DT; ++t) {
-          const uint16_t* vr = &vt[(32 * t + l32) * C::VLD + kcol];
-          const uint2 v0 = *reinterpret_cast<const uint2*>(vr);
-          const uint2 v1 = *reinterpret_cast<const uint2*>(vr + 8);
+          const int d = 32 * t + l32;
+          const uint2 v0 = *reinterpret_cast<const uint2*>(&vt[vt_off<BLK>(d, kc)]);
+          const uint2 v1 = *reinterpret_cast<const uint2*>(&vt[vt_off<BLK>(d, kc + 8)]);
           const uint4 vu = make_uint4(v0.x, v0.y, v1.x, v1.y);
           acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vu), pb, acc_o[t], 0, 0, 0);
         }
       }
 
-    it = it_next;
+    // ---- stage the next tile, prefetch the one after, swap buffers
+    if (nxt >= 0) {
+      store_tile(stage ^ 1);
+      const int it_nn = next_valid(it_n + 1, nn);
+      if (nn >= 0) load_tile(nn);
+      it_n = it_nn;
+    } else {
+      nn = -1;
+    }
+    __syncthreads();
     cur = nxt;
+    nxt = nn;
+    stage ^= 1;
   }
 
-  // ---- epilogue
-  if (q_ok) {
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    uint16_t* op = a.o + (bh * a.lq + q_row) * D;
+  // ---- merge the two key halves of each query slice, then write O and lse
+  l_run = half_swap_sum(l_run);  // both lane halves now hold the slice's partial sum
+  float* mrg = reinterpret_cast<float*>(smem);  // [NQS][2 + 16 DT][64] floats; tile buffers are free now
+  constexpr int MR = 2 + 16 * C::DT;
+  static_assert(C::NQS * MR * 64 * 4 <= 2 * C::STAGE * 2, "merge buffer fits in LDS");
+  float* my = mrg + qs * MR * 64;
+  if (kh == 1) {
+    my[0 * 64 + lane] = m_run;
+    my[1 * 64 + lane] = l_run;
 #pragma unroll
     for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int d = 32 * t + 8 * g + 4 * hh;
-        uint2 w;
-        w.x = pack_bf16(acc_o[t][4 * g + 0] * inv, acc_o[t][4 * g + 1] * inv);
-        w.y = pack_bf16(acc_o[t][4 * g + 2] * inv, acc_o[t][4 * g + 3] * inv);
-        *reinterpret_cast<uint2*>(op + d) = w;
-      }
-    if (a.lse != nullptr && hh == 0)
-      a.lse[bh * a.lq + q_row] = le_run > 0.f ? (m_run + log2f(le_run)) * 0.69314718055994530942f : -INFINITY;
+      for (int e = 0; e < 16; ++e) my[(2 + 16 * t + e) * 64 + lane] = acc_o[t][e];
+  }
+  __syncthreads();
+  if (kh == 0) {
+    const float m1 = my[0 * 64 + lane], l1 = my[1 * 64 + lane];
+    const float mm = fmaxf(m_run, m1);
+    const float a0 = m_run == -INFINITY ? 0.f : exp2f(m_run - mm);
+    const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - mm);
+    const float l = l_run * a0 + l1 * a1;
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    if (q_ok) {
+      uint16_t* op = a.o + (bh * a.lq + q_row) * D;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int d = 32 * t + 8 * g + 4 * hh;
+          float o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            o[e] = (acc_o[t][4 * g + e] * a0 + my[(2 + 16 * t + 4 * g + e) * 64 + lane] * a1) * inv;
+          uint2 w;
+          w.x = pack_bf16(o[0], o[1]);
+          w.y = pack_bf16(o[2], o[3]);
+          *reinterpret_cast<uint2*>(op + d) = w;
+        }
+      if (a.lse != nullptr && hh == 0)
+        a.lse[bh * a.lq + q_row] = l > 0.f ? (mm + log2f(l)) * 0.69314718055994530942f : -INFINITY;
+    }
   }
 }
 

@@ -77,10 +77,16 @@ def check_gap_rule(gpu_list, oracle_row_scores, keep, sel, k):
     return "tolerant"
 
 
-def check_output(o_gpu: np.ndarray, o_ref: np.ndarray, lse_gpu=None, lse_ref=None, what=""):
+# Sharpened-softmax stress cases (scale 4 / sqrt(D)): few keys dominate, so the
+# bf16 rounding of P (relative 2^-9) shows directly, |dO| <= 2^-9 max|v| + the
+# bf16 rounding of O (2^-9 |O|); with |v|, |O| <= 4 that is <= 1.6e-2.
+O_MAX_ABS_SHARP = 1.6e-2
+
+
+def check_output(o_gpu: np.ndarray, o_ref: np.ndarray, lse_gpu=None, lse_ref=None, what="", max_abs=O_MAX_ABS):
     """O: max-abs and per-head relative Frobenius; lse: max-abs.  Arrays [.., L, D]."""
     d = np.abs(o_gpu - o_ref)
-    assert d.max() <= O_MAX_ABS, f"{what}: max |dO| = {d.max():.3e}"
+    assert d.max() <= max_abs, f"{what}: max |dO| = {d.max():.3e}"
     num = np.sqrt(((o_gpu - o_ref) ** 2).sum(axis=(-2, -1)))
     den = np.sqrt((o_ref ** 2).sum(axis=(-2, -1)))
     rel = num / np.maximum(den, 1e-30)
