@@ -5,25 +5,28 @@
 // time and that head's K/V (74 MB at the 720p shape) stays resident in the
 // 256 MB last-level cache.  The work-group has 2 * BLK/32 wavefronts: wave w
 // owns the 32-row query slice (w % (BLK/32)) and the key half (w / (BLK/32)) of
-// every key block, so each wave touches only half of each K and V tile and the
-// work-group keeps two waves per SIMD resident (<= 256 VGPRs each).
+// every key block, so each wave touches only half of each K and V tile and two
+// waves per SIMD stay resident (<= 256 VGPRs each).
 //
 // Per key block of the query block's ascending list:
-//   * the K tile (BLK x D) is stored row-major in LDS (16-byte row padding) and
-//     the V tile transposed (D x BLK) in an XOR-swizzled layout whose 8-byte
-//     chunks are bank-conflict-free both for the transposing writes and for the
-//     MFMA operand reads.  LDS is double-buffered: the tile of step t+1 is written
-//     while step t computes, so there is one barrier per step, and the global
+//   * K and V tiles (BLK x D each) are copied row-major into LDS with coalesced
+//     16-byte loads and stores (row pitches padded so that the operand reads
+//     below are bank-conflict-free).  LDS is double-buffered: the tile of step
+//     t+1 is written while step t computes (one barrier per step) and the global
 //     loads of step t+2 are in flight during the whole step;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (fp32 accumulate).  The
 //     transpose leaves each lane holding 16 keys of ONE query column -- exactly
 //     the B-operand layout P^T needs -- so the softmax state is lane-local up to
 //     one cross-half (lane l <-> l+32) max per step (v_permlane32_swap);
-//   * online softmax in the log2 domain with the scale folded into one FMA,
-//     and lazy rescaling: O and l are only rescaled when a query's running
-//     maximum grows by more than 2^8 (P then stays <= 256, exact enough in fp32
-//     and bf16), which skips nearly all rescales after the first steps;
-//   * O^T += V^T P^T on the same MFMA (P rounded to bf16 once).
+//   * online softmax in the log2 domain: the scale is folded into one FMA, the
+//     exponential is the bare v_exp_f32, and O is rescaled lazily, only when a
+//     query's running maximum grows by more than 2^8 (P then stays <= 256,
+//     harmless in fp32 and bf16), which skips nearly all rescales;
+//   * O^T += V^T P^T on the same MFMA (P rounded to bf16 once).  The V^T
+//     operand comes straight from the row-major V tile through the LDS
+//     transpose read ds_read_b64_tr_b16 (in each 16-lane group, source lane s
+//     points at V[r0 + s/4][4 (c0 + s%4)], and lane j receives
+//     V[r0 .. r0+3][4 c0 + j]: 4 keys of one d column).
 // The two key halves of a query slice each hold a partial (m, l, O); they are
 // merged once through LDS at the end.  O = O^T / l in bf16, lse = ln2*(m + log2 l).
 //
@@ -33,10 +36,17 @@
 //   C[m][n]: n = l % 32, m = 8 (a / 4) + 4h + (a % 4), accumulator a = 0..15
 // A and B only need to agree on k, so keys may be permuted consistently: the
 // P^T operand reuses the S^T C layout directly, and the V^T operand reads the
-// same key permutation from LDS.
+// same key permutation.
+#include <type_traits>
+
 #include "device_common.h"
 
 namespace sparstar {
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 template <int D, int BLK>
 struct AttnCfg {
@@ -47,23 +57,16 @@ struct AttnCfg {
   static constexpr int KT = KH / 32;          // 32-key sub-tiles per wave and step
   static constexpr int DS = D / 16;           // MFMA k-steps over D
   static constexpr int DT = D / 32;           // 32-row d tiles of O^T
-  static constexpr int KLD = D + 8;           // K tile row pitch in bf16 (16-byte pad)
+  static constexpr int KLD = D + 8;           // K row pitch (bf16): consecutive rows 4 banks apart
+  static constexpr int VLD = D + 16;          // V row pitch (bf16): consecutive rows 8 banks apart
   static constexpr int K_ELEMS = BLK * KLD;
-  static constexpr int V_ELEMS = D * BLK;     // V^T rows of BLK keys, swizzled, unpadded
+  static constexpr int V_ELEMS = BLK * VLD;
   static constexpr int STAGE = K_ELEMS + V_ELEMS;
-  static constexpr int KCH = BLK * D / 8 / NT;   // 16-byte K chunks per thread
-  static constexpr int VG = BLK * D / 32;        // (4 keys x 8 d) V groups per tile
-  static_assert(KCH * NT * 8 == BLK * D, "K tile split");
-  static_assert(VG <= NT, "one V group per thread at most");
+  static constexpr int CPR = D / 8;                 // 16-byte chunks per row
+  static constexpr int CH = BLK * CPR / NT;         // chunks per thread, for each of K and V
+  static constexpr int ROWS_PER_PASS = NT / CPR;    // rows covered by one chunk pass
+  static_assert(CH * NT == BLK * CPR, "tile split");
 };
-
-// Element offset of V^T[d][key] in the swizzled layout: rows of BLK keys whose
-// 4-key (8-byte) chunks are permuted by f(d) = ((d >> 3) & 15) ^ ((d & 7) << 1).
-template <int BLK>
-__device__ __forceinline__ int vt_off(int d, int key) {
-  const int f = ((d >> 3) & 15) ^ ((d & 7) << 1);
-  return d * BLK + (((key >> 2) ^ f) << 2) + (key & 3);
-}
 
 __device__ __forceinline__ float half_swap_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -73,6 +76,15 @@ __device__ __forceinline__ float half_swap_max(float x) {
 __device__ __forceinline__ float half_swap_sum(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
+}
+
+__device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(const_cast<uint16_t*>(p)));
 }
 
 template <int D, int BLK, bool DENSE>
@@ -134,59 +146,49 @@ void attn_fwd_kernel(AttnArgs a) {
   float m_run = -INFINITY;  // running max (log2 domain), shared by both lane halves
   float l_run = 0.f;        // this lane's partial row sum (its 16 keys per sub-tile)
 
-  // ---- global -> register prefetch and register -> LDS store of one tile
-  uint4 kreg[C::KCH];
-  uint4 vreg[4];
+  // ---- tile copy: thread tid moves chunk (row0 + p * ROWS_PER_PASS, col) of K and V, p = 0..CH-1
+  const int row0 = tid / C::CPR, col8 = (tid % C::CPR) * 8;
+  const int goff = row0 * D + col8;
+  uint4 kreg[C::CH], vreg[C::CH];
   auto load_tile = [&](int blk) {
     const int64_t key0 = (int64_t)blk * BLK;
+    const uint16_t* kt = kbase + key0 * D + goff;
+    const uint16_t* vtg = vbase + key0 * D + goff;
+    if (key0 + BLK <= a.lk) {
 #pragma unroll
-    for (int r = 0; r < C::KCH; ++r) {
-      const int c = tid + C::NT * r;
-      const int row = c / (D / 8), col = c % (D / 8);
-      const int64_t key = key0 + row;
-      kreg[r] = key < a.lk ? *reinterpret_cast<const uint4*>(kbase + key * D + col * 8) : make_uint4(0, 0, 0, 0);
-    }
-    if (tid < C::VG) {
-      const int dg = tid % (D / 8), kg = tid / (D / 8);
+      for (int p = 0; p < C::CH; ++p) {
+        kreg[p] = *reinterpret_cast<const uint4*>(kt + p * C::ROWS_PER_PASS * D);
+        vreg[p] = *reinterpret_cast<const uint4*>(vtg + p * C::ROWS_PER_PASS * D);
+      }
+    } else {  // the partial last block: rows past Lk read as zeros
+      const int64_t rows = a.lk - key0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t key = key0 + 4 * kg + e;
-        vreg[e] = key < a.lk ? *reinterpret_cast<const uint4*>(vbase + key * D + dg * 8) : make_uint4(0, 0, 0, 0);
+      for (int p = 0; p < C::CH; ++p) {
+        const bool ok = row0 + p * C::ROWS_PER_PASS < rows;
+        kreg[p] = ok ? *reinterpret_cast<const uint4*>(kt + p * C::ROWS_PER_PASS * D) : make_uint4(0, 0, 0, 0);
+        vreg[p] = ok ? *reinterpret_cast<const uint4*>(vtg + p * C::ROWS_PER_PASS * D) : make_uint4(0, 0, 0, 0);
       }
     }
   };
+  uint16_t* const kst = smem + row0 * C::KLD + col8;
+  uint16_t* const vst = smem + C::K_ELEMS + row0 * C::VLD + col8;
   auto store_tile = [&](int stage) {
-    uint16_t* ks = smem + stage * C::STAGE;
-    uint16_t* vt = ks + C::K_ELEMS;
 #pragma unroll
-    for (int r = 0; r < C::KCH; ++r) {
-      const int c = tid + C::NT * r;
-      const int row = c / (D / 8), col = c % (D / 8);
-      *reinterpret_cast<uint4*>(&ks[row * C::KLD + col * 8]) = kreg[r];
-    }
-    if (tid < C::VG) {
-      const int dg = tid % (D / 8), kg = tid / (D / 8);
-      const uint32_t w0[4] = {vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w};
-      const uint32_t w1[4] = {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w};
-      const uint32_t w2[4] = {vreg[2].x, vreg[2].y, vreg[2].z, vreg[2].w};
-      const uint32_t w3[4] = {vreg[3].x, vreg[3].y, vreg[3].z, vreg[3].w};
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        // d = 8 dg + 2p (low halves) and 8 dg + 2p + 1 (high halves); keys 4 kg .. 4 kg + 3
-        uint2 lo, hi;
-        lo.x = (w0[p] & 0xffffu) | (w1[p] << 16);
-        lo.y = (w2[p] & 0xffffu) | (w3[p] << 16);
-        hi.x = (w0[p] >> 16) | (w1[p] & 0xffff0000u);
-        hi.y = (w2[p] >> 16) | (w3[p] & 0xffff0000u);
-        *reinterpret_cast<uint2*>(&vt[vt_off<BLK>(8 * dg + 2 * p, 4 * kg)]) = lo;
-        *reinterpret_cast<uint2*>(&vt[vt_off<BLK>(8 * dg + 2 * p + 1, 4 * kg)]) = hi;
-      }
+    for (int p = 0; p < C::CH; ++p) {
+      *reinterpret_cast<uint4*>(kst + stage * C::STAGE + p * C::ROWS_PER_PASS * C::KLD) = kreg[p];
+      *reinterpret_cast<uint4*>(vst + stage * C::STAGE + p * C::ROWS_PER_PASS * C::VLD) = vreg[p];
     }
   };
 
+  // per-lane LDS read bases (stage 0)
+  const uint16_t* const k_rd = smem + (kh * C::KH + l32) * C::KLD + 8 * hh;
+  const int grp = lane >> 4, sl = lane & 15;
+  const uint16_t* const v_rd =
+      smem + C::K_ELEMS + (kh * C::KH + 4 * hh + (sl >> 2)) * C::VLD + 16 * (grp & 1) + 4 * (sl & 3);
+
   int cur, nxt, nn;
-  int it = next_valid(0, cur);
-  int it_n = next_valid(it + 1, nxt);
+  const int it0 = next_valid(0, cur);
+  int it_n = next_valid(it0 + 1, nxt);
   if (cur >= 0) {
     load_tile(cur);
     store_tile(0);
@@ -195,10 +197,11 @@ void attn_fwd_kernel(AttnArgs a) {
   __syncthreads();
 
   const float sl2 = a.scale_log2;
-  int stage = 0;
-  while (cur >= 0) {
-    const uint16_t* ks = smem + stage * C::STAGE;
-    const uint16_t* vt = ks + C::K_ELEMS;
+
+  auto step = [&](auto stage_c) {
+    constexpr int ST = decltype(stage_c)::value;
+    const uint16_t* ks = k_rd + ST * C::STAGE;
+    const uint16_t* vs = v_rd + ST * C::STAGE;
 
     // ---- S^T = K Q^T for this wave's keys
     f32x16 acc_s[C::KT];
@@ -206,10 +209,9 @@ void attn_fwd_kernel(AttnArgs a) {
     for (int kt = 0; kt < C::KT; ++kt) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc_s[kt][e] = 0.f;
-      const uint16_t* kr = &ks[(kh * C::KH + kt * 32 + l32) * C::KLD + 8 * hh];
 #pragma unroll
       for (int s = 0; s < C::DS; ++s) {
-        const uint4 u = *reinterpret_cast<const uint4*>(kr + 16 * s);
+        const uint4 u = *reinterpret_cast<const uint4*>(ks + kt * 32 * C::KLD + 16 * s);
         acc_s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u), qf[s], acc_s[kt], 0, 0, 0);
       }
     }
@@ -235,7 +237,7 @@ void attn_fwd_kernel(AttnArgs a) {
     mx = half_swap_max(mx) * sl2;  // this step's max logit (log2 domain) for the lane's query
     if (__any(mx > m_run + 8.0f)) {
       const float m_new = fmaxf(m_run, mx);
-      const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+      const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t)
@@ -249,9 +251,9 @@ void attn_fwd_kernel(AttnArgs a) {
     for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; e += 2) {
-        const float p0 = exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
-        const float p1 = exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
-        pk[kt][e / 2] = pack_bf16(p0, p1);
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
+        pk[kt][e / 2] = pack2_bf16(p0, p1);
         l_run += p0 + p1;
       }
 
@@ -262,27 +264,28 @@ void attn_fwd_kernel(AttnArgs a) {
       for (int half = 0; half < 2; ++half) {
         // accumulators a = 8 half + i of sub-tile kt hold keys
         //   base + 4 hh + i (i = 0..3) and base + 8 + 4 hh + (i - 4) (i = 4..7),
-        // base = kh * KH + 32 kt + 16 half
+        // base = kh * KH + 32 kt + 16 half; the two transpose reads fetch the
+        // same keys of V for d = 32 t + l % 32.
         uint4 pu;
         pu.x = pk[kt][4 * half + 0];
         pu.y = pk[kt][4 * half + 1];
         pu.z = pk[kt][4 * half + 2];
         pu.w = pk[kt][4 * half + 3];
         const bf16x8 pb = __builtin_bit_cast(bf16x8, pu);
-        const int kc = kh * C::KH + 32 * kt + 16 * half + 4 * hh;
 #pragma unroll
         for (int t = 0; t < C::DT; ++t) {
-          const int d = 32 * t + l32;
-          const uint2 v0 = *reinterpret_cast<const uint2*>(&vt[vt_off<BLK>(d, kc)]);
-          const uint2 v1 = *reinterpret_cast<const uint2*>(&vt[vt_off<BLK>(d, kc + 8)]);
-          const uint4 vu = make_uint4(v0.x, v0.y, v1.x, v1.y);
-          acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vu), pb, acc_o[t], 0, 0, 0);
+          const uint16_t* vr = vs + (32 * kt + 16 * half) * C::VLD + 32 * t;
+          const s16x4 v0 = lds_read_tr(vr);
+          const s16x4 v1 = lds_read_tr(vr + 8 * C::VLD);
+          const s16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+          const bf16x8 va = __builtin_bit_cast(bf16x8, vv);
+          acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc_o[t], 0, 0, 0);
         }
       }
 
     // ---- stage the next tile, prefetch the one after, swap buffers
     if (nxt >= 0) {
-      store_tile(stage ^ 1);
+      store_tile(ST ^ 1);
       const int it_nn = next_valid(it_n + 1, nn);
       if (nn >= 0) load_tile(nn);
       it_n = it_nn;
@@ -292,7 +295,12 @@ void attn_fwd_kernel(AttnArgs a) {
     __syncthreads();
     cur = nxt;
     nxt = nn;
-    stage ^= 1;
+  };
+
+  while (cur >= 0) {
+    step(std::integral_constant<int, 0>{});
+    if (cur < 0) break;
+    step(std::integral_constant<int, 1>{});
   }
 
   // ---- merge the two key halves of each query slice, then write O and lse
@@ -329,8 +337,8 @@ void attn_fwd_kernel(AttnArgs a) {
           for (int e = 0; e < 4; ++e)
             o[e] = (acc_o[t][4 * g + e] * a0 + my[(2 + 16 * t + 4 * g + e) * 64 + lane] * a1) * inv;
           uint2 w;
-          w.x = pack_bf16(o[0], o[1]);
-          w.y = pack_bf16(o[2], o[3]);
+          w.x = pack2_bf16(o[0], o[1]);
+          w.y = pack2_bf16(o[2], o[3]);
           *reinterpret_cast<uint2*>(op + d) = w;
         }
       if (a.lse != nullptr && hh == 0)
