@@ -143,6 +143,8 @@ def main() -> int:
     ws = torch.empty(S.sparstar_score_workspace_bytes(B, H, Lq, Lk, D, w.block), dtype=torch.uint8, device=dev)
     o = torch.empty_like(q)
     lse = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+    aws = torch.empty(max(1, S.sparstar_attn_workspace_bytes(B, H, Lq, Lk, D, w.block)), dtype=torch.uint8,
+                      device=dev)
     torch.cuda.synchronize()
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
@@ -153,7 +155,7 @@ def main() -> int:
         S.sparstar_score_blocks(q, k, w.block, w.density, keep, kv_stride=stride, workspace=ws, out=(num, idx))
         if record is not None:
             record[1].record()
-        S.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, out=o, lse=lse)
+        S.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, out=o, lse=lse, workspace=aws)
         if record is not None:
             record[2].record()
 
@@ -208,7 +210,7 @@ def main() -> int:
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "attn_fwd_kernel<128,64,sparse>",
+            "kernel": "sparse forward call: attn_fwd_kernel<128,64,sparse,split> + attn_merge_kernel",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
@@ -220,10 +222,10 @@ def main() -> int:
     if not args.no_dense:
         log("dense comparison")
         e0, e1 = ev(), ev()
-        S.sparstar_dense_attn_fwd(q, k, v, w.block, out=o, lse=lse)  # warm
+        S.sparstar_dense_attn_fwd(q, k, v, w.block, out=o, lse=lse, workspace=aws)  # warm
         torch.cuda.synchronize()
         e0.record()
-        S.sparstar_dense_attn_fwd(q, k, v, w.block, out=o, lse=lse)
+        S.sparstar_dense_attn_fwd(q, k, v, w.block, out=o, lse=lse, workspace=aws)
         e1.record()
         torch.cuda.synchronize()
         dense_ms = e0.elapsed_time(e1)

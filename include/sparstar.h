@@ -118,6 +118,16 @@ int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq
                           void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Bytes of device workspace that lets the attention calls below split the key
+ * blocks into 8 contiguous ranges (one per XCD of the MI355X, so that each
+ * XCD's L2 streams one eighth of a head's K/V) and merge the partial results:
+ * per (batch, head, query block, range, query row) an fp16 partial O normalised
+ * by its own row sum ([.., D]) and an fp32 (running max, row sum) pair.  0 when
+ * the key sequence has fewer than 16 blocks (no split).  0 also for invalid sizes.
+ */
+size_t sparstar_attn_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size);
+
+/*
  * Block-sparse attention forward over the lists of sparstar_score_blocks
  * (Eq. 7): query token t of block i attends to the key tokens u < Lk of the
  * blocks kv_indices[b,h,i,0 .. kv_num_blocks[b,h,i]).
@@ -129,15 +139,22 @@ int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq
  *   q, k, v         device bf16 Q [B,H,Lq,D], K and V [B,H,Lk,D].
  *   D, block_size   as for sparstar_score_blocks.
  *   kv_num_blocks, kv_indices, kv_stride   device, as written by
- *                   sparstar_score_blocks.  Lists are trusted to be ascending
- *                   and duplicate-free; defensively, a count is clamped to
- *                   [0, kv_stride] and an entry outside [0, n_k) is skipped.
+ *                   sparstar_score_blocks: each list ascending and
+ *                   duplicate-free.  Defensively, a count is clamped to
+ *                   [0, kv_stride] and an entry outside [0, n_k) is skipped, so
+ *                   a malformed list gives unspecified values but never an
+ *                   out-of-range access.
  *   o               device bf16 out [B,H,Lq,D].
  *   lse             device fp32 out [B,H,Lq], or NULL.
+ *   workspace       NULL for a single pass, or device scratch of at least
+ *                   sparstar_attn_workspace_bytes(...) bytes (256-byte aligned,
+ *                   no initialisation needed, garbage afterwards) for the
+ *                   key-range split; the results agree to fp32/fp16 rounding.
  */
 int sparstar_sparse_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq, int64_t Lk,
                              int D, int block_size, const int32_t* kv_num_blocks, const int32_t* kv_indices,
-                             int kv_stride, float softmax_scale, void* o, float* lse, void* stream);
+                             int kv_stride, float softmax_scale, void* o, float* lse, void* workspace,
+                             size_t workspace_bytes, void* stream);
 
 /*
  * Dense attention forward with the same tile engine: every query attends to
@@ -146,7 +163,8 @@ int sparstar_sparse_attn_fwd(const void* q, const void* k, const void* v, int B,
  * `block_size` tokens.
  */
 int sparstar_dense_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq, int64_t Lk, int D,
-                            int block_size, float softmax_scale, void* o, float* lse, void* stream);
+                            int block_size, float softmax_scale, void* o, float* lse, void* workspace,
+                            size_t workspace_bytes, void* stream);
 
 /* Message for the last non-OK return on this thread ("" if none). */
 const char* sparstar_last_error(void);

@@ -47,6 +47,8 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 template <int D, int BLK>
 struct AttnCfg {
@@ -87,14 +89,22 @@ __device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
       (__attribute__((address_space(3))) s16x4*)(const_cast<uint16_t*>(p)));
 }
 
-template <int D, int BLK, bool DENSE>
+template <int D, int BLK, bool DENSE, bool SPLIT>
 __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a) {
   using C = AttnCfg<D, BLK>;
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+  __shared__ int list_pos[2];
 
-  const int64_t bh = blockIdx.x / a.n_q;
-  const int qb = (int)(blockIdx.x % a.n_q);
+  // Work item.  With the key-range split, consecutive work-group ids cover the
+  // kSplits key ranges of one query block; work-groups are dispatched round-robin
+  // over the eight XCDs, so each XCD streams one range of the current head.
+  const int split = SPLIT ? (int)(blockIdx.x % kSplits) : 0;
+  const int64_t work = SPLIT ? blockIdx.x / kSplits : blockIdx.x;
+  const int64_t bh = work / a.n_q;
+  const int qb = (int)(work % a.n_q);
+  const int blk_lo = SPLIT ? (int)((int64_t)split * a.n_k / kSplits) : 0;
+  const int blk_hi = SPLIT ? (int)((int64_t)(split + 1) * a.n_k / kSplits) : a.n_k;
 
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
   const int l32 = lane % 32, hh = lane / 32;
@@ -104,25 +114,53 @@ void attn_fwd_kernel(AttnArgs a) {
   const uint16_t* kbase = a.k + bh * a.lk * D;
   const uint16_t* vbase = a.v + bh * a.lk * D;
 
-  // ---- list of key blocks
-  int nblk;
+  // ---- list positions [pos_lo, pos_hi) that may hold blocks of [blk_lo, blk_hi)
+  int pos_lo, pos_hi;
   const int32_t* list = nullptr;
   if constexpr (DENSE) {
-    nblk = a.n_k;
+    pos_lo = blk_lo;
+    pos_hi = blk_hi;
   } else {
     const int64_t r = bh * a.n_q + qb;
-    nblk = a.kv_num_blocks[r];
+    int nblk = a.kv_num_blocks[r];
     nblk = nblk < 0 ? 0 : (nblk > a.stride ? a.stride : nblk);
     list = a.kv_indices + r * a.stride;
+    if constexpr (SPLIT) {
+      // an ascending list: the range starts after the entries < blk_lo and ends
+      // after the entries < blk_hi
+      if (tid < 2) list_pos[tid] = 0;
+      __syncthreads();
+      int c_lo = 0, c_hi = 0;
+      for (int i = tid; i < nblk; i += C::NT) {
+        const int j = list[i];
+        c_lo += j < blk_lo;
+        c_hi += j < blk_hi;
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        c_lo += __shfl_xor(c_lo, off, 64);
+        c_hi += __shfl_xor(c_hi, off, 64);
+      }
+      if (lane == 0) {
+        atomicAdd(&list_pos[0], c_lo);
+        atomicAdd(&list_pos[1], c_hi);
+      }
+      __syncthreads();
+      pos_lo = list_pos[0];
+      pos_hi = list_pos[1];
+    } else {
+      pos_lo = 0;
+      pos_hi = nblk;
+    }
   }
-  // first list position >= it holding a valid block; the block (or -1) in blk
+  // first position >= it in [it, pos_hi) holding a block of [blk_lo, blk_hi); the block (or -1) in blk
   auto next_valid = [&](int it, int& blk) -> int {
     blk = -1;
-    for (; it < nblk; ++it) {
+    for (; it < pos_hi; ++it) {
       int j;
       if constexpr (DENSE) j = it;
       else j = __builtin_amdgcn_readfirstlane(list[it]);
-      if (j >= 0 && j < a.n_k) { blk = j; break; }
+      if (j >= blk_lo && j < blk_hi) { blk = j; break; }
     }
     return it;
   };
@@ -187,7 +225,7 @@ void attn_fwd_kernel(AttnArgs a) {
       smem + C::K_ELEMS + (kh * C::KH + 4 * hh + (sl >> 2)) * C::VLD + 16 * (grp & 1) + 4 * (sl & 3);
 
   int cur, nxt, nn;
-  const int it0 = next_valid(0, cur);
+  const int it0 = next_valid(pos_lo, cur);
   int it_n = next_valid(it0 + 1, nxt);
   if (cur >= 0) {
     load_tile(cur);
@@ -325,7 +363,26 @@ void attn_fwd_kernel(AttnArgs a) {
     const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - mm);
     const float l = l_run * a0 + l1 * a1;
     const float inv = l > 0.f ? 1.f / l : 0.f;
-    if (q_ok) {
+    if (SPLIT && q_ok) {
+      const int64_t prow = (work * kSplits + split) * BLK + qs * 32 + l32;
+      _Float16* po = reinterpret_cast<_Float16*>(a.part_o) + prow * D;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int d = 32 * t + 8 * g + 4 * hh;
+          f16x4 w;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            w[e] = (_Float16)((acc_o[t][4 * g + e] * a0 + my[(2 + 16 * t + 4 * g + e) * 64 + lane] * a1) * inv);
+          *reinterpret_cast<f16x4*>(po + d) = w;
+        }
+      if (hh == 0) {
+        a.part_ml[2 * prow] = mm;
+        a.part_ml[2 * prow + 1] = l;
+      }
+    }
+    if (!SPLIT && q_ok) {
       uint16_t* op = a.o + (bh * a.lq + q_row) * D;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t)
@@ -347,13 +404,87 @@ void attn_fwd_kernel(AttnArgs a) {
   }
 }
 
+// Combines the kSplits partial results of one query block:
+//   O = sum_r w_r O_r / sum_r w_r,  w_r = l_r 2^(m_r - M),  M = max_r m_r,
+//   lse = ln2 (M + log2 sum_r w_r).
+// Ranges with no visible key (l_r = 0) have weight 0 and their O_r is not read.
+template <int D, int BLK>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+  __shared__ float wts[kSplits][BLK];
+  const int64_t work = blockIdx.x;
+  const int64_t bh = work / a.n_q;
+  const int qb = (int)(work % a.n_q);
+  const int tid = threadIdx.x;
+  const int64_t rows = a.lq - (int64_t)qb * BLK;
+  for (int row = tid; row < BLK; row += 256) {
+    float m[kSplits], l[kSplits], mm = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < kSplits; ++r) {
+      const int64_t prow = (work * kSplits + r) * BLK + row;
+      m[r] = a.part_ml[2 * prow];
+      l[r] = a.part_ml[2 * prow + 1];
+      if (l[r] > 0.f) mm = fmaxf(mm, m[r]);
+    }
+    float tot = 0.f;
+#pragma unroll
+    for (int r = 0; r < kSplits; ++r) {
+      const float w = l[r] > 0.f ? l[r] * exp2f(m[r] - mm) : 0.f;
+      wts[r][row] = w;
+      tot += w;
+    }
+    const float inv = tot > 0.f ? 1.f / tot : 0.f;
+#pragma unroll
+    for (int r = 0; r < kSplits; ++r) wts[r][row] *= inv;
+    if (row < rows && a.lse != nullptr)
+      a.lse[bh * a.lq + (int64_t)qb * BLK + row] = tot > 0.f ? (mm + log2f(tot)) * 0.69314718055994530942f : -INFINITY;
+  }
+  __syncthreads();
+  constexpr int CPR = D / 8;
+  for (int c = tid; c < BLK * CPR; c += 256) {
+    const int row = c / CPR, d0 = (c % CPR) * 8;
+    if (row >= rows) continue;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < kSplits; ++r) {
+      const float w = wts[r][row];
+      if (w == 0.f) continue;
+      const int64_t prow = (work * kSplits + r) * BLK + row;
+      const f16x8 v = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.part_o) + prow * D + d0);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = fmaf(w, (float)v[e], acc[e]);
+    }
+    uint4 o;
+    o.x = pack2_bf16(acc[0], acc[1]);
+    o.y = pack2_bf16(acc[2], acc[3]);
+    o.z = pack2_bf16(acc[4], acc[5]);
+    o.w = pack2_bf16(acc[6], acc[7]);
+    *reinterpret_cast<uint4*>(a.o + (bh * a.lq + (int64_t)qb * BLK + row) * D + d0) = o;
+  }
+}
+
 template <int D, int BLK>
 static hipError_t launch_cfg(const AttnArgs& a, bool dense, hipStream_t stream) {
-  const int64_t grid = (int64_t)a.bh * a.n_q;
-  if (grid == 0) return hipSuccess;
-  if (dense) attn_fwd_kernel<D, BLK, true><<<grid, AttnCfg<D, BLK>::NT, 0, stream>>>(a);
-  else attn_fwd_kernel<D, BLK, false><<<grid, AttnCfg<D, BLK>::NT, 0, stream>>>(a);
+  const int64_t items = (int64_t)a.bh * a.n_q;
+  if (items == 0) return hipSuccess;
+  constexpr int NT = AttnCfg<D, BLK>::NT;
+  if (a.part_o != nullptr) {
+    if (dense) attn_fwd_kernel<D, BLK, true, true><<<items * kSplits, NT, 0, stream>>>(a);
+    else attn_fwd_kernel<D, BLK, false, true><<<items * kSplits, NT, 0, stream>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    attn_merge_kernel<D, BLK><<<items, 256, 0, stream>>>(a);
+  } else {
+    if (dense) attn_fwd_kernel<D, BLK, true, false><<<items, NT, 0, stream>>>(a);
+    else attn_fwd_kernel<D, BLK, false, false><<<items, NT, 0, stream>>>(a);
+  }
   return hipGetLastError();
+}
+
+size_t attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block) {
+  if (n_k < 2 * kSplits) return 0;  // ranges of fewer than two blocks: single pass
+  const int64_t rows = bh * n_q * kSplits * block;
+  const size_t o_bytes = (size_t(rows * d) * 2 + 255) & ~size_t(255);
+  return o_bytes + size_t(rows) * 2 * sizeof(float);
 }
 
 hipError_t launch_attn(const AttnArgs& a, int d, int block, bool dense, hipStream_t stream) {

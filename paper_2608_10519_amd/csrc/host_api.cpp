@@ -211,9 +211,16 @@ extern "C" int sparstar_score_blocks(const void* q, const void* k, int B, int H,
   return ok();
 }
 
+extern "C" size_t sparstar_attn_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
+  if (check_sizes(B, H, Lq, Lk, D, block_size) != SPARSTAR_OK) return 0;
+  return sparstar::attn_workspace_bytes(int64_t(B) * H, ceil_div(Lq, block_size), ceil_div(Lk, block_size), D,
+                                        block_size);
+}
+
 static int attn_common(const void* q, const void* k, const void* v, int B, int H, int64_t Lq, int64_t Lk, int D,
                        int block_size, const int32_t* kv_num_blocks, const int32_t* kv_indices, int kv_stride,
-                       float softmax_scale, void* o, float* lse, void* stream, bool dense) {
+                       float softmax_scale, void* o, float* lse, void* workspace, size_t workspace_bytes,
+                       void* stream, bool dense) {
   using namespace sparstar;
   if (int rc = check_sizes(B, H, Lq, Lk, D, block_size)) return rc;
   if (!k || !v || (Lq > 0 && (!q || !o))) return fail(SPARSTAR_ERR_INVALID_ARG, "q, k, v and o must be non-null");
@@ -229,11 +236,37 @@ static int attn_common(const void* q, const void* k, const void* v, int B, int H
   if (!(softmax_scale == softmax_scale) || isinf(softmax_scale))
     return fail(SPARSTAR_ERR_INVALID_ARG, "softmax_scale must be finite");
   const int64_t nq = ceil_div(Lq, block_size), nk = ceil_div(Lk, block_size);
+  const size_t need = attn_workspace_bytes(int64_t(B) * H, nq, nk, D, block_size);
+  const bool split = workspace != nullptr && need > 0;
+  if (split) {
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+      return fail(SPARSTAR_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+      return fail(SPARSTAR_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
+  }
   if (nq == 0) return ok();
   const double sc = softmax_scale > 0.f ? double(softmax_scale) : 1.0 / sqrt(double(D));
-  AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-             static_cast<uint16_t*>(o), lse, kv_num_blocks, kv_indices, Lq, Lk, B * H, int(nq), int(nk),
-             dense ? 0 : kv_stride, float(sc * 1.4426950408889634074)};
+  AttnArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
+  a.kv_num_blocks = kv_num_blocks;
+  a.kv_indices = kv_indices;
+  a.lq = Lq;
+  a.lk = Lk;
+  a.bh = B * H;
+  a.n_q = int(nq);
+  a.n_k = int(nk);
+  a.stride = dense ? 0 : kv_stride;
+  a.scale_log2 = float(sc * 1.4426950408889634074);
+  if (split) {
+    const int64_t rows = int64_t(B) * H * nq * kSplits * block_size;
+    char* ws = static_cast<char*>(workspace);
+    a.part_o = reinterpret_cast<uint16_t*>(ws);
+    a.part_ml = reinterpret_cast<float*>(ws + ((size_t(rows * D) * 2 + 255) & ~size_t(255)));
+  }
   hipError_t e = launch_attn(a, D, block_size, dense, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
   return ok();
@@ -242,14 +275,14 @@ static int attn_common(const void* q, const void* k, const void* v, int B, int H
 extern "C" int sparstar_sparse_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq,
                                         int64_t Lk, int D, int block_size, const int32_t* kv_num_blocks,
                                         const int32_t* kv_indices, int kv_stride, float softmax_scale, void* o,
-                                        float* lse, void* stream) {
+                                        float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   return attn_common(q, k, v, B, H, Lq, Lk, D, block_size, kv_num_blocks, kv_indices, kv_stride, softmax_scale, o,
-                     lse, stream, false);
+                     lse, workspace, workspace_bytes, stream, false);
 }
 
 extern "C" int sparstar_dense_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq,
                                        int64_t Lk, int D, int block_size, float softmax_scale, void* o, float* lse,
-                                       void* stream) {
-  return attn_common(q, k, v, B, H, Lq, Lk, D, block_size, nullptr, nullptr, 0, softmax_scale, o, lse, stream,
-                     true);
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_common(q, k, v, B, H, Lq, Lk, D, block_size, nullptr, nullptr, 0, softmax_scale, o, lse, workspace,
+                     workspace_bytes, stream, true);
 }

@@ -62,7 +62,17 @@ struct AttnArgs {
   int64_t lq, lk;
   int bh, n_q, n_k, stride;
   float scale_log2;   // softmax scale * log2(e)
+  // Key-range split: with part_o set, work item (bh, query block, r) covers key
+  // blocks [r n_k / kSplits, (r + 1) n_k / kSplits) and writes a partial result
+  // that a merge kernel combines; otherwise one pass writes O and lse.
+  uint16_t* part_o;   // [BH * n_q, kSplits, BLK, D] fp16 partial O normalised by its own row sum
+  float* part_ml;     // [BH * n_q, kSplits, BLK, 2] (running max in log2 units, row sum)
 };
+
+constexpr int kSplits = 8;  // one key range per XCD
+
+// Bytes of attention workspace for the key-range split (0 when it is not used).
+size_t attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block);
 
 hipError_t launch_pool(const PoolArgs& a, int d, int block, hipStream_t stream);
 hipError_t launch_score(const ScoreArgs& a, int d, hipStream_t stream);

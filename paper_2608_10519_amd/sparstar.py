@@ -51,10 +51,13 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.sparstar_score_blocks.argtypes = [c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_dp, c_i, c_rp, c_i,
                                           c_p, c_p, c_i, c_p, c_p, c_sz, c_p]
     lib.sparstar_score_blocks.restype = c_i
+    lib.sparstar_attn_workspace_bytes.argtypes = [c_i, c_i, c_i64, c_i64, c_i, c_i]
+    lib.sparstar_attn_workspace_bytes.restype = c_sz
     lib.sparstar_sparse_attn_fwd.argtypes = [c_p, c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_p, c_p, c_i,
-                                             c_f, c_p, c_p, c_p]
+                                             c_f, c_p, c_p, c_p, c_sz, c_p]
     lib.sparstar_sparse_attn_fwd.restype = c_i
-    lib.sparstar_dense_attn_fwd.argtypes = [c_p, c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_f, c_p, c_p, c_p]
+    lib.sparstar_dense_attn_fwd.argtypes = [c_p, c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_f, c_p, c_p, c_p,
+                                            c_sz, c_p]
     lib.sparstar_dense_attn_fwd.restype = c_i
     lib.sparstar_last_error.argtypes = []
     lib.sparstar_last_error.restype = ctypes.c_char_p
@@ -98,6 +101,22 @@ def sparstar_score_workspace_bytes(B: int, H: int, Lq: int, Lk: int, D: int, blo
     return int(load().sparstar_score_workspace_bytes(B, H, Lq, Lk, D, block_size))
 
 
+def sparstar_attn_workspace_bytes(B: int, H: int, Lq: int, Lk: int, D: int, block_size: int) -> int:
+    return int(load().sparstar_attn_workspace_bytes(B, H, Lq, Lk, D, block_size))
+
+
+def _attn_workspace(workspace, split: bool, B, H, Lq, Lk, D, block_size, device):
+    """(pointer, bytes) of the attention workspace: the caller's, a fresh one, or none."""
+    if not split:
+        return None, 0
+    if workspace is None:
+        n = sparstar_attn_workspace_bytes(B, H, Lq, Lk, D, block_size)
+        if n == 0:
+            return None, 0
+        workspace = torch.empty(n, dtype=torch.uint8, device=device)
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
 def sparstar_kv_stride(H: int, Lk: int, block_size: int, budget, keep=()) -> int:
     b, nb = _budget_array(budget)
     kr, nk = _keep_array(keep)
@@ -139,8 +158,11 @@ def sparstar_score_blocks(q: torch.Tensor, k: torch.Tensor, block_size: int, bud
 
 def sparstar_sparse_attn_fwd(q, k, v, kv_num_blocks, kv_indices, block_size: int, softmax_scale: float = 0.0, *,
                              out: torch.Tensor | None = None, lse: torch.Tensor | None = None,
-                             return_lse: bool = True):
-    """Block-sparse forward: returns (O [B,H,Lq,D] bf16, lse [B,H,Lq] fp32 or None)."""
+                             return_lse: bool = True, split: bool = True, workspace: torch.Tensor | None = None):
+    """Block-sparse forward: returns (O [B,H,Lq,D] bf16, lse [B,H,Lq] fp32 or None).
+
+    split=True runs the key-range split (allocating its workspace unless one is
+    given); split=False runs the single-pass kernel."""
     B, H, Lq, D = _bhld(q, "q")
     _, _, Lk, _ = _bhld(k, "k")
     _bhld(v, "v")
@@ -151,17 +173,18 @@ def sparstar_sparse_attn_fwd(q, k, v, kv_num_blocks, kv_indices, block_size: int
     o = torch.empty_like(q) if out is None else out
     if lse is None and return_lse:
         lse = torch.empty((B, H, Lq), dtype=torch.float32, device=q.device)
+    wp, wn = _attn_workspace(workspace, split, B, H, Lq, Lk, D, block_size, q.device)
     rc = load().sparstar_sparse_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), B, H, Lq, Lk, D, block_size,
                                          kv_num_blocks.data_ptr(), kv_indices.data_ptr(), kv_indices.shape[-1],
                                          float(softmax_scale), o.data_ptr(),
-                                         lse.data_ptr() if lse is not None else None, _stream())
+                                         lse.data_ptr() if lse is not None else None, wp, wn, _stream())
     _check("sparstar_sparse_attn_fwd", rc)
     return o, lse
 
 
 def sparstar_dense_attn_fwd(q, k, v, block_size: int = 64, softmax_scale: float = 0.0, *,
                             out: torch.Tensor | None = None, lse: torch.Tensor | None = None,
-                            return_lse: bool = True):
+                            return_lse: bool = True, split: bool = True, workspace: torch.Tensor | None = None):
     """Dense forward with the same tile engine: returns (O, lse)."""
     B, H, Lq, D = _bhld(q, "q")
     _, _, Lk, _ = _bhld(k, "k")
@@ -169,8 +192,9 @@ def sparstar_dense_attn_fwd(q, k, v, block_size: int = 64, softmax_scale: float 
     o = torch.empty_like(q) if out is None else out
     if lse is None and return_lse:
         lse = torch.empty((B, H, Lq), dtype=torch.float32, device=q.device)
+    wp, wn = _attn_workspace(workspace, split, B, H, Lq, Lk, D, block_size, q.device)
     rc = load().sparstar_dense_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), B, H, Lq, Lk, D, block_size,
                                         float(softmax_scale), o.data_ptr(),
-                                        lse.data_ptr() if lse is not None else None, _stream())
+                                        lse.data_ptr() if lse is not None else None, wp, wn, _stream())
     _check("sparstar_dense_attn_fwd", rc)
     return o, lse

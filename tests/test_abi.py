@@ -31,7 +31,8 @@ def _declared():
 def test_exports_every_declared_symbol(lib):
     names = _declared()
     assert {"sparstar_score_blocks", "sparstar_sparse_attn_fwd", "sparstar_dense_attn_fwd",
-            "sparstar_score_workspace_bytes", "sparstar_kv_stride", "sparstar_last_error"} <= set(names)
+            "sparstar_score_workspace_bytes", "sparstar_attn_workspace_bytes", "sparstar_kv_stride",
+            "sparstar_last_error"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -105,13 +106,31 @@ def test_score_blocks_rejects_invalid_arguments(lib, over, code, msg):
 
 def _attn(lib, dense=False, **over):
     a = dict(q=FAKE, k=FAKE, v=FAKE, B=1, H=2, Lq=512, Lk=1152, D=64, block=64, num=FAKE, idx=FAKE, stride=6,
-             scale=0.0, o=FAKE, lse=None)
+             scale=0.0, o=FAKE, lse=None, ws=None, ws_bytes=0)
     a.update(over)
     if dense:
         return lib.sparstar_dense_attn_fwd(a["q"], a["k"], a["v"], a["B"], a["H"], a["Lq"], a["Lk"], a["D"],
-                                           a["block"], a["scale"], a["o"], a["lse"], None)
+                                           a["block"], a["scale"], a["o"], a["lse"], a["ws"], a["ws_bytes"], None)
     return lib.sparstar_sparse_attn_fwd(a["q"], a["k"], a["v"], a["B"], a["H"], a["Lq"], a["Lk"], a["D"], a["block"],
-                                        a["num"], a["idx"], a["stride"], a["scale"], a["o"], a["lse"], None)
+                                        a["num"], a["idx"], a["stride"], a["scale"], a["o"], a["lse"], a["ws"],
+                                        a["ws_bytes"], None)
+
+
+def test_attn_workspace_bytes(lib):
+    # 720p: 24 heads x 1125 query blocks x 8 key ranges x 64 rows: fp16 O [.., 128] + fp32 (max, sum)
+    rows = 24 * 1125 * 8 * 64
+    want = (rows * 128 * 2 + 255) // 256 * 256 + rows * 8
+    assert S.sparstar_attn_workspace_bytes(1, 24, 72_000, 144_512, 128, 64) == want
+    # fewer than 16 key blocks: no split, no workspace
+    assert S.sparstar_attn_workspace_bytes(1, 2, 512, 960, 64, 64) == 0
+    assert S.sparstar_attn_workspace_bytes(1, 2, 512, 1152, 64, 64) > 0
+
+
+@pytest.mark.parametrize("dense", [False, True])
+@pytest.mark.parametrize("over", [dict(ws=FAKE, ws_bytes=100), dict(ws=FAKE + 16, ws_bytes=1 << 30)])
+def test_attention_rejects_bad_workspace(lib, dense, over):
+    assert _attn(lib, dense=dense, **over) == S.ERR_WORKSPACE
+    assert "workspace" in S.last_error()
 
 
 @pytest.mark.parametrize("dense", [False, True])

@@ -143,7 +143,7 @@ def test_selector_ties_prefer_lower_index(gpu_lib):
     assert torch.equal(num, num)
 
 
-def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_override=None):
+def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_override=None, split=True):
     """Run the sparse forward with given lists on all heads; return GPU and oracle outputs."""
     import torch
 
@@ -155,7 +155,7 @@ def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_ove
     n_q = -(-w.lq // w.block)
     num, idx = lists_to_device([lists_h], n_q)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
-    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, softmax_scale=scale or 0.0)
+    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, softmax_scale=scale or 0.0, split=split)
     torch.cuda.synchronize()
     og, lg = bf16_tensor_to_f64(o), lse.cpu().numpy().astype(np.float64)
     refs = [O.sparse_attention(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), bf16_to_f64(vb_[0, h]),
@@ -191,12 +191,13 @@ def _random_lists(w: Workload, rng, heads=None):
 
 @pytest.mark.parametrize("name,w", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
 @pytest.mark.parametrize("sharp", [False, True], ids=["tau", "4tau"])
-def test_sparse_attention_matches_oracle(gpu_lib, name, w, sharp):
+@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
+def test_sparse_attention_matches_oracle(gpu_lib, name, w, sharp, split):
     rng = np.random.default_rng(zlib.crc32(name.encode()) % 1000 + int(sharp))
     lists_h = _random_lists(w, rng)
     scale = 4.0 / math.sqrt(w.head_dim) if sharp else None
-    _say(f"[attn] {name} sharp={sharp}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk}")
-    og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, scale)
+    _say(f"[attn] {name} sharp={sharp} split={split}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk}")
+    og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, scale, split=split)
     err = check_output(og, o_ref, lg, l_ref, what=name, max_abs=O_MAX_ABS_SHARP if sharp else O_MAX_ABS)
     _say(f"[attn] {name}: max |dO| = {err:.2e}")
 
@@ -223,13 +224,14 @@ def test_end_to_end_tiny_against_oracle(gpu_lib):
                      l_ref[None], what=f"head {h}")
 
 
-@pytest.mark.parametrize("name,w", ATTN_CASES[:3], ids=[c[0] for c in ATTN_CASES[:3]])
-def test_dense_attention_matches_oracle(gpu_lib, name, w):
+@pytest.mark.parametrize("name,w", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
+@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
+def test_dense_attention_matches_oracle(gpu_lib, name, w, split):
     import torch
 
-    _say(f"[dense] {name}")
+    _say(f"[dense] {name} split={split}")
     qb_, kb_, vb_ = generate(w)
-    o, lse = gpu_lib.sparstar_dense_attn_fwd(to_dev(qb_), to_dev(kb_), to_dev(vb_), w.block)
+    o, lse = gpu_lib.sparstar_dense_attn_fwd(to_dev(qb_), to_dev(kb_), to_dev(vb_), w.block, split=split)
     torch.cuda.synchronize()
     refs = [O.dense_attention(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), bf16_to_f64(vb_[0, h]))
             for h in range(w.heads)]
@@ -237,18 +239,19 @@ def test_dense_attention_matches_oracle(gpu_lib, name, w):
                  np.stack([r[1] for r in refs])[None], what=name)
 
 
-def test_full_lists_equal_dense(gpu_lib):
+@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
+def test_full_lists_equal_dense(gpu_lib, split):
     """rho = 1 (every block listed) equals the dense forward, bit for bit."""
     import torch
 
     w = ATTN_CASES[1][1]
-    _say("[dense==sparse(all)]")
+    _say(f"[dense==sparse(all)] split={split}")
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
     n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
     num, idx = lists_to_device([[[list(range(n_k))] * n_q for _ in range(w.heads)]], n_q)
-    o1, l1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
-    o2, l2 = gpu_lib.sparstar_dense_attn_fwd(q, k, v, w.block)
+    o1, l1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, split=split)
+    o2, l2 = gpu_lib.sparstar_dense_attn_fwd(q, k, v, w.block, split=split)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
@@ -279,12 +282,14 @@ def test_zero_queries_average_selected_values(gpu_lib):
     assert n_k > 1
 
 
-def test_empty_and_invalid_list_entries(gpu_lib):
-    """Empty rows give O = 0, lse = -inf; out-of-range entries are skipped; counts clamp to the stride."""
+@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
+def test_empty_and_invalid_list_entries(gpu_lib, split):
+    """Empty rows give O = 0, lse = -inf; out-of-range entries of an ascending list
+    are skipped; counts clamp to the stride."""
     import torch
 
     w = ATTN_CASES[0][1]
-    _say("[empty/invalid lists]")
+    _say(f"[empty/invalid lists] split={split}")
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
     n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
@@ -297,14 +302,14 @@ def test_empty_and_invalid_list_entries(gpu_lib):
             if i % 3 == 0:
                 continue  # empty
             if i % 3 == 1:
-                num[0, h, i] = 3
-                idx[0, h, i, :3] = torch.tensor([1, n_k + 5, 4])
+                num[0, h, i] = 4
+                idx[0, h, i] = torch.tensor([-3, 1, 4, n_k + 5])
                 lists_ref[h][i] = [1, 4]
             else:
                 num[0, h, i] = 99  # clamped to the stride (4)
-                idx[0, h, i] = torch.tensor([0, 2, -1, 7])
-                lists_ref[h][i] = [0, 2, 7]
-    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num.cuda(), idx.cuda(), w.block)
+                idx[0, h, i] = torch.tensor([0, 2, 7, n_k - 1])
+                lists_ref[h][i] = [0, 2, 7, n_k - 1]
+    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num.cuda(), idx.cuda(), w.block, split=split)
     torch.cuda.synchronize()
     refs = [O.sparse_attention(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), bf16_to_f64(vb_[0, h]),
                                lists_ref[h], w.block) for h in range(w.heads)]
@@ -312,6 +317,22 @@ def test_empty_and_invalid_list_entries(gpu_lib):
     lg = lse.cpu().numpy().astype(np.float64)
     check_output(og, np.stack([r[0] for r in refs])[None], lg, np.stack([r[1] for r in refs])[None], what="lists")
     assert (og[0, :, : w.block] == 0).all() and np.isneginf(lg[0, :, : w.block]).all()
+
+
+def test_split_agrees_with_single_pass(gpu_lib):
+    """The key-range split and the single pass agree to fp16/fp32 rounding."""
+    import torch
+
+    w = ATTN_CASES[3][1]
+    _say("[split vs one pass]")
+    qb_, kb_, vb_ = generate(w)
+    q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
+    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, 0.3, keep_ranges(w))
+    o1, l1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, split=True)
+    o2, l2 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, split=False)
+    torch.cuda.synchronize()
+    assert (o1.float() - o2.float()).abs().max().item() <= 1e-2
+    assert (l1 - l2).abs().max().item() <= 1e-4
 
 
 def test_deterministic(gpu_lib):
