@@ -119,11 +119,12 @@ int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq
 
 /*
  * Bytes of device workspace that lets the attention calls below split the key
- * blocks into 8 contiguous ranges (one per XCD of the MI355X, so that each
- * XCD's L2 streams one eighth of a head's K/V) and merge the partial results:
- * per (batch, head, query block, range, query row) an fp16 partial O normalised
- * by its own row sum ([.., D]) and an fp32 (running max, row sum) pair.  0 when
- * the key sequence has fewer than 16 blocks (no split).  0 also for invalid sizes.
+ * blocks of every query block into 16 contiguous ranges (two per XCD of the
+ * MI355X, taken one after the other, so that each XCD's L2 streams about one
+ * sixteenth of a head's K/V at a time) and merge the partial results: per
+ * (batch, head, query block, range, query row) an fp16 partial O normalised by
+ * its own row sum ([.., D]) and an fp32 (running max, row sum) pair.  0 when
+ * the key sequence has fewer than 16 blocks (no split), and for invalid sizes.
  */
 size_t sparstar_attn_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size);
 

@@ -89,18 +89,39 @@ __device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
       (__attribute__((address_space(3))) s16x4*)(const_cast<uint16_t*>(p)));
 }
 
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  // raw (stride 0) buffer; reads past `bytes` return zeros
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
 template <int D, int BLK, bool DENSE, bool SPLIT>
 __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a) {
   using C = AttnCfg<D, BLK>;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+  // K double buffer, then V double buffer.  Step t reads K of tile t+1 (for the
+  // scores one step ahead) and V of tile t, while K of t+2 and V of t+1 are
+  // written into the other halves.
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::K_ELEMS + 2 * C::V_ELEMS];
   __shared__ int list_pos[2];
 
-  // Work item.  With the key-range split, consecutive work-group ids cover the
-  // kSplits key ranges of one query block; work-groups are dispatched round-robin
-  // over the eight XCDs, so each XCD streams one range of the current head.
-  const int split = SPLIT ? (int)(blockIdx.x % kSplits) : 0;
-  const int64_t work = SPLIT ? blockIdx.x / kSplits : blockIdx.x;
+  // Work item.  Work-groups are dispatched round-robin over the eight XCDs, so
+  // with the key-range split the work-group id decodes as
+  //   id = ((bh * S + s) * n_q + qb) * 8 + x,  range r = 8 s + x,  S = kSplits / 8:
+  // XCD x runs range x of every query block of head bh, then range 8 + x, ...,
+  // and its L2 holds one range of the head's K/V at a time.
+  int split = 0;
+  int64_t work = blockIdx.x;
+  if constexpr (SPLIT) {
+    constexpr int S = kSplits / 8;
+    const int64_t x = blockIdx.x % 8, rest = blockIdx.x / 8;
+    const int64_t qbi = rest % a.n_q, rest2 = rest / a.n_q;
+    split = (int)((rest2 % S) * 8 + x);
+    work = (rest2 / S) * a.n_q + qbi;
+  }
   const int64_t bh = work / a.n_q;
   const int qb = (int)(work % a.n_q);
   const int blk_lo = SPLIT ? (int)((int64_t)split * a.n_k / kSplits) : 0;
@@ -110,9 +131,6 @@ void attn_fwd_kernel(AttnArgs a) {
   const int l32 = lane % 32, hh = lane / 32;
   const int qs = wave % C::NQS;   // query slice
   const int kh = wave / C::NQS;   // key half
-
-  const uint16_t* kbase = a.k + bh * a.lk * D;
-  const uint16_t* vbase = a.v + bh * a.lk * D;
 
   // ---- list positions [pos_lo, pos_hi) that may hold blocks of [blk_lo, blk_hi)
   int pos_lo, pos_hi;
@@ -153,16 +171,28 @@ void attn_fwd_kernel(AttnArgs a) {
       pos_hi = nblk;
     }
   }
-  // first position >= it in [it, pos_hi) holding a block of [blk_lo, blk_hi); the block (or -1) in blk
-  auto next_valid = [&](int it, int& blk) -> int {
-    blk = -1;
-    for (; it < pos_hi; ++it) {
-      int j;
-      if constexpr (DENSE) j = it;
-      else j = __builtin_amdgcn_readfirstlane(list[it]);
-      if (j >= blk_lo && j < blk_hi) { blk = j; break; }
+
+  // ---- block cursor: the next list entry is prefetched one call ahead with a
+  // vector-memory load, so its latency hides behind a whole step
+  int cur_pos = pos_lo;
+  // (the range check covers the vector offset, so the position goes there:
+  // reading one past the end returns 0 instead of touching memory)
+  const __amdgpu_buffer_rsrc_t list_rs = make_rsrc(list, DENSE ? 0u : (uint32_t)pos_hi * 4u);
+  uint32_t pf = 0;
+  if constexpr (!DENSE) pf = __builtin_amdgcn_raw_buffer_load_b32(list_rs, (uint32_t)cur_pos * 4u, 0u, 0);
+  // next block of [blk_lo, blk_hi) in list order, or -1
+  auto fetch_next = [&]() -> int {
+    if constexpr (DENSE) {
+      return cur_pos < pos_hi ? cur_pos++ : -1;
+    } else {
+      while (cur_pos < pos_hi) {
+        const int j = __builtin_amdgcn_readfirstlane((int)pf);
+        ++cur_pos;
+        pf = __builtin_amdgcn_raw_buffer_load_b32(list_rs, (uint32_t)cur_pos * 4u, 0u, 0);
+        if (j >= blk_lo && j < blk_hi) return j;
+      }
+      return -1;
     }
-    return it;
   };
 
   // ---- Q fragment (B operand of S^T = K Q^T): Q[q][16 s + 8 hh .. +7]
@@ -182,80 +212,103 @@ void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc_o[t][e] = 0.f;
   float m_run = -INFINITY;  // running max (log2 domain), shared by both lane halves
-  float l_run = 0.f;        // this lane's partial row sum (its 16 keys per sub-tile)
+  float l_run = 0.f;        // this lane's partial row sum of the bf16 P it applied
 
-  // ---- tile copy: thread tid moves chunk (row0 + p * ROWS_PER_PASS, col) of K and V, p = 0..CH-1
+  // ---- tile copy through buffer loads: thread tid moves chunk
+  // (row0 + p * ROWS_PER_PASS, col8) of a tile.  Each tile gets its own
+  // descriptor (base at the tile, records = bytes left in the head), so rows
+  // past Lk read as zeros; the per-lane offsets stay in the range-checked
+  // vector offset.
   const int row0 = tid / C::CPR, col8 = (tid % C::CPR) * 8;
-  const int goff = row0 * D + col8;
+  const uint16_t* const kbase = a.k + bh * a.lk * D;
+  const uint16_t* const vbase = a.v + bh * a.lk * D;
+  constexpr uint32_t TILE_BYTES = BLK * D * 2;
+  uint32_t voff[C::CH];
+#pragma unroll
+  for (int p = 0; p < C::CH; ++p) voff[p] = (uint32_t)((row0 + p * C::ROWS_PER_PASS) * D + col8) * 2u;
+  auto tile_bytes = [&](int blk) -> uint32_t {
+    const int64_t left = (a.lk - (int64_t)blk * BLK) * D * 2;
+    return left < TILE_BYTES ? (uint32_t)left : TILE_BYTES;
+  };
   uint4 kreg[C::CH], vreg[C::CH];
-  auto load_tile = [&](int blk) {
-    const int64_t key0 = (int64_t)blk * BLK;
-    const uint16_t* kt = kbase + key0 * D + goff;
-    const uint16_t* vtg = vbase + key0 * D + goff;
-    if (key0 + BLK <= a.lk) {
+  auto load_k = [&](int blk) {
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(kbase + (int64_t)blk * BLK * D, tile_bytes(blk));
 #pragma unroll
-      for (int p = 0; p < C::CH; ++p) {
-        kreg[p] = *reinterpret_cast<const uint4*>(kt + p * C::ROWS_PER_PASS * D);
-        vreg[p] = *reinterpret_cast<const uint4*>(vtg + p * C::ROWS_PER_PASS * D);
-      }
-    } else {  // the partial last block: rows past Lk read as zeros
-      const int64_t rows = a.lk - key0;
+    for (int p = 0; p < C::CH; ++p) kreg[p] = buf_load16(rs, voff[p], 0u);
+  };
+  auto load_v = [&](int blk) {
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(vbase + (int64_t)blk * BLK * D, tile_bytes(blk));
 #pragma unroll
-      for (int p = 0; p < C::CH; ++p) {
-        const bool ok = row0 + p * C::ROWS_PER_PASS < rows;
-        kreg[p] = ok ? *reinterpret_cast<const uint4*>(kt + p * C::ROWS_PER_PASS * D) : make_uint4(0, 0, 0, 0);
-        vreg[p] = ok ? *reinterpret_cast<const uint4*>(vtg + p * C::ROWS_PER_PASS * D) : make_uint4(0, 0, 0, 0);
-      }
-    }
+    for (int p = 0; p < C::CH; ++p) vreg[p] = buf_load16(rs, voff[p], 0u);
   };
   uint16_t* const kst = smem + row0 * C::KLD + col8;
-  uint16_t* const vst = smem + C::K_ELEMS + row0 * C::VLD + col8;
-  auto store_tile = [&](int stage) {
+  uint16_t* const vst = smem + 2 * C::K_ELEMS + row0 * C::VLD + col8;
+  auto store_k = [&](int buf) {
 #pragma unroll
-    for (int p = 0; p < C::CH; ++p) {
-      *reinterpret_cast<uint4*>(kst + stage * C::STAGE + p * C::ROWS_PER_PASS * C::KLD) = kreg[p];
-      *reinterpret_cast<uint4*>(vst + stage * C::STAGE + p * C::ROWS_PER_PASS * C::VLD) = vreg[p];
-    }
+    for (int p = 0; p < C::CH; ++p)
+      *reinterpret_cast<uint4*>(kst + buf * C::K_ELEMS + p * C::ROWS_PER_PASS * C::KLD) = kreg[p];
+  };
+  auto store_v = [&](int buf) {
+#pragma unroll
+    for (int p = 0; p < C::CH; ++p)
+      *reinterpret_cast<uint4*>(vst + buf * C::V_ELEMS + p * C::ROWS_PER_PASS * C::VLD) = vreg[p];
   };
 
-  // per-lane LDS read bases (stage 0)
+  // per-lane LDS read bases (buffer 0)
   const uint16_t* const k_rd = smem + (kh * C::KH + l32) * C::KLD + 8 * hh;
   const int grp = lane >> 4, sl = lane & 15;
   const uint16_t* const v_rd =
-      smem + C::K_ELEMS + (kh * C::KH + 4 * hh + (sl >> 2)) * C::VLD + 16 * (grp & 1) + 4 * (sl & 3);
+      smem + 2 * C::K_ELEMS + (kh * C::KH + 4 * hh + (sl >> 2)) * C::VLD + 16 * (grp & 1) + 4 * (sl & 3);
 
-  int cur, nxt, nn;
-  const int it0 = next_valid(pos_lo, cur);
-  int it_n = next_valid(it0 + 1, nxt);
-  if (cur >= 0) {
-    load_tile(cur);
-    store_tile(0);
-    if (nxt >= 0) load_tile(nxt);
-  }
-  __syncthreads();
-
-  const float sl2 = a.scale_log2;
-
-  auto step = [&](auto stage_c) {
-    constexpr int ST = decltype(stage_c)::value;
-    const uint16_t* ks = k_rd + ST * C::STAGE;
-    const uint16_t* vs = v_rd + ST * C::STAGE;
-
-    // ---- S^T = K Q^T for this wave's keys
-    f32x16 acc_s[C::KT];
+  // ---- S^T = K Q^T for this wave's keys of the K tile in buffer kb
+  auto scores = [&](int kb, f32x16* acc) {
+    const uint16_t* ks = k_rd + kb * C::K_ELEMS;
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc_s[kt][e] = 0.f;
+      for (int e = 0; e < 16; ++e) acc[kt][e] = 0.f;
 #pragma unroll
       for (int s = 0; s < C::DS; ++s) {
         const uint4 u = *reinterpret_cast<const uint4*>(ks + kt * 32 * C::KLD + 16 * s);
-        acc_s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u), qf[s], acc_s[kt], 0, 0, 0);
+        acc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u), qf[s], acc[kt], 0, 0, 0);
       }
     }
+  };
 
-    // ---- keys >= Lk (only in a partial last block) are masked
-    const int64_t key0 = (int64_t)cur * BLK;
+  // ---- prologue: K of tiles 0 and 1 and V of tile 0 staged, K of tile 2 and
+  // V of tile 1 in flight, S of tile 0 computed
+  int b0 = fetch_next();
+  int b1 = fetch_next();
+  int b2 = fetch_next();
+  f32x16 acc_s[C::KT];
+  if (b0 >= 0) {
+    load_k(b0);
+    load_v(b0);
+    store_k(0);
+    store_v(0);
+  }
+  if (b1 >= 0) {
+    load_k(b1);
+    store_k(1);
+    load_v(b1);
+  }
+  if (b2 >= 0) load_k(b2);
+  __syncthreads();
+  if (b0 >= 0) scores(0, acc_s);
+  __syncthreads();  // K buffer 0 is rewritten in the first step
+
+  const float sl2 = a.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // one step: softmax and O += P V of tile t (block b0) while the scores of
+  // tile t+1 (block b1) run on the matrix cores
+  auto step = [&](auto parity) {
+    constexpr int P = decltype(parity)::value;
+    f32x16 acc_n[C::KT];
+    if (b1 >= 0) scores(1 - P, acc_n);
+
+    // keys >= Lk (only in a partial last block) are masked
+    const int64_t key0 = (int64_t)b0 * BLK;
     if (key0 + BLK > a.lk) {
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt)
@@ -266,7 +319,7 @@ void attn_fwd_kernel(AttnArgs a) {
         }
     }
 
-    // ---- online softmax with lazy rescaling
+    // online softmax with lazy rescaling
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt)
@@ -291,11 +344,13 @@ void attn_fwd_kernel(AttnArgs a) {
       for (int e = 0; e < 16; e += 2) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
-        pk[kt][e / 2] = pack2_bf16(p0, p1);
-        l_run += p0 + p1;
+        const bf16x2 pp = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
+        pk[kt][e / 2] = __builtin_bit_cast(uint32_t, pp);
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l_run, false);
       }
 
-    // ---- O^T += V^T P^T over 16-key k-steps
+    // O^T += V^T P^T over 16-key k-steps (V tile of block b0 in buffer P)
+    const uint16_t* vs = v_rd + P * C::V_ELEMS;
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
@@ -316,28 +371,27 @@ void attn_fwd_kernel(AttnArgs a) {
           const s16x4 v0 = lds_read_tr(vr);
           const s16x4 v1 = lds_read_tr(vr + 8 * C::VLD);
           const s16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-          const bf16x8 va = __builtin_bit_cast(bf16x8, vv);
-          acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, acc_o[t], 0, 0, 0);
+          acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, acc_o[t], 0, 0, 0);
         }
       }
 
-    // ---- stage the next tile, prefetch the one after, swap buffers
-    if (nxt >= 0) {
-      store_tile(ST ^ 1);
-      const int it_nn = next_valid(it_n + 1, nn);
-      if (nn >= 0) load_tile(nn);
-      it_n = it_nn;
-    } else {
-      nn = -1;
-    }
+    // stage K of t+2 and V of t+1, start the loads of K of t+3 and V of t+2
+    if (b2 >= 0) store_k(P);
+    if (b1 >= 0) store_v(1 - P);
+    const int b3 = fetch_next();
+    if (b3 >= 0) load_k(b3);
+    if (b2 >= 0) load_v(b2);
     __syncthreads();
-    cur = nxt;
-    nxt = nn;
+#pragma unroll
+    for (int kt = 0; kt < C::KT; ++kt) acc_s[kt] = acc_n[kt];
+    b0 = b1;
+    b1 = b2;
+    b2 = b3;
   };
 
-  while (cur >= 0) {
+  while (b0 >= 0) {
     step(std::integral_constant<int, 0>{});
-    if (cur < 0) break;
+    if (b0 < 0) break;
     step(std::integral_constant<int, 1>{});
   }
 
@@ -345,7 +399,7 @@ void attn_fwd_kernel(AttnArgs a) {
   l_run = half_swap_sum(l_run);  // both lane halves now hold the slice's partial sum
   float* mrg = reinterpret_cast<float*>(smem);  // [NQS][2 + 16 DT][64] floats; tile buffers are free now
   constexpr int MR = 2 + 16 * C::DT;
-  static_assert(C::NQS * MR * 64 * 4 <= 2 * C::STAGE * 2, "merge buffer fits in LDS");
+  static_assert(C::NQS * MR * 64 * 4 <= (2 * C::K_ELEMS + 2 * C::V_ELEMS) * 2, "merge buffer fits in LDS");
   float* my = mrg + qs * MR * 64;
   if (kh == 1) {
     my[0 * 64 + lane] = m_run;
@@ -481,7 +535,7 @@ static hipError_t launch_cfg(const AttnArgs& a, bool dense, hipStream_t stream) 
 }
 
 size_t attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block) {
-  if (n_k < 2 * kSplits) return 0;  // ranges of fewer than two blocks: single pass
+  if (n_k < kSplits) return 0;  // fewer key blocks than ranges: single pass
   const int64_t rows = bh * n_q * kSplits * block;
   const size_t o_bytes = (size_t(rows * d) * 2 + 255) & ~size_t(255);
   return o_bytes + size_t(rows) * 2 * sizeof(float);

@@ -69,7 +69,9 @@ struct AttnArgs {
   float* part_ml;     // [BH * n_q, kSplits, BLK, 2] (running max in log2 units, row sum)
 };
 
-constexpr int kSplits = 8;  // one key range per XCD
+// Key ranges per query block: kSplits / 8 consecutive ranges per XCD, so that
+// each XCD's 4 MB L2 holds about one range of a head's K/V at a time.
+constexpr int kSplits = 16;
 
 // Bytes of attention workspace for the key-range split (0 when it is not used).
 size_t attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block);

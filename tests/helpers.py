@@ -8,7 +8,10 @@ import numpy as np
 GAP = 1e-3          # selection: exact match required where the boundary gap exceeds this
 O_MAX_ABS = 1e-2    # output: max |dO| (bf16 inputs, fp32-accumulated reference)
 O_REL_FRO = 1e-2    # output: per-head relative Frobenius error
-LSE_ABS = 1e-3      # log-sum-exp: max |dlse|
+# log-sum-exp: max |dlse|.  The kernel's row sum is taken over the bf16-rounded P
+# it applies to V (each p within a relative 2^-8 of the exact value), so lse can
+# be off by up to ln(1 + 2^-8) = 3.9e-3.
+LSE_ABS = 4e-3
 
 
 def to_dev(bits: np.ndarray):
@@ -81,9 +84,11 @@ def check_gap_rule(gpu_list, oracle_row_scores, keep, sel, k):
 # bf16 rounding of P (relative 2^-9) shows directly, |dO| <= 2^-9 max|v| + the
 # bf16 rounding of O (2^-9 |O|); with |v|, |O| <= 4 that is <= 1.6e-2.
 O_MAX_ABS_SHARP = 1.6e-2
+LSE_ABS_SHARP = LSE_ABS
 
 
-def check_output(o_gpu: np.ndarray, o_ref: np.ndarray, lse_gpu=None, lse_ref=None, what="", max_abs=O_MAX_ABS):
+def check_output(o_gpu: np.ndarray, o_ref: np.ndarray, lse_gpu=None, lse_ref=None, what="", max_abs=O_MAX_ABS,
+                 lse_abs=LSE_ABS):
     """O: max-abs and per-head relative Frobenius; lse: max-abs.  Arrays [.., L, D]."""
     d = np.abs(o_gpu - o_ref)
     assert d.max() <= max_abs, f"{what}: max |dO| = {d.max():.3e}"
@@ -96,5 +101,5 @@ def check_output(o_gpu: np.ndarray, o_ref: np.ndarray, lse_gpu=None, lse_ref=Non
         assert (np.isfinite(lse_gpu) == fin).all(), f"{what}: lse finiteness differs"
         if fin.any():
             dl = np.abs(lse_gpu[fin] - lse_ref[fin]).max()
-            assert dl <= LSE_ABS, f"{what}: max |dlse| = {dl:.3e}"
+            assert dl <= lse_abs, f"{what}: max |dlse| = {dl:.3e}"
     return float(d.max())

@@ -4,7 +4,7 @@ Small cases are compared element by element; they span several tiles and a
 ragged tail.  Tolerances (tests/helpers.py): selection exact where the oracle's
 boundary gap exceeds 1e-3 (tie-tolerant otherwise), scores |dS| <= 1e-5(1+|S|),
 pooled blocks |d| <= 1e-5, O max-abs <= 1e-2 plus relative Frobenius <= 1e-2 per
-head, lse max-abs <= 1e-3.
+head, lse max-abs <= 4e-3 (the row sum is over bf16-rounded P).
 """
 from __future__ import annotations
 
@@ -17,7 +17,7 @@ import pytest
 
 import oracle as O
 from synthetic import TINY, Workload, bf16_to_f64, generate, keep_ranges
-from tests.helpers import (O_MAX_ABS, O_MAX_ABS_SHARP, bf16_tensor_to_f64, check_gap_rule, check_output,
+from tests.helpers import (LSE_ABS, LSE_ABS_SHARP, O_MAX_ABS, O_MAX_ABS_SHARP, bf16_tensor_to_f64, check_gap_rule, check_output,
                            lists_from_device, lists_to_device, to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -198,7 +198,8 @@ def test_sparse_attention_matches_oracle(gpu_lib, name, w, sharp, split):
     scale = 4.0 / math.sqrt(w.head_dim) if sharp else None
     _say(f"[attn] {name} sharp={sharp} split={split}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk}")
     og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, scale, split=split)
-    err = check_output(og, o_ref, lg, l_ref, what=name, max_abs=O_MAX_ABS_SHARP if sharp else O_MAX_ABS)
+    err = check_output(og, o_ref, lg, l_ref, what=name, max_abs=O_MAX_ABS_SHARP if sharp else O_MAX_ABS,
+                       lse_abs=LSE_ABS_SHARP if sharp else LSE_ABS)
     _say(f"[attn] {name}: max |dO| = {err:.2e}")
 
 
@@ -263,9 +264,8 @@ def test_unit_values_give_unit_output(gpu_lib):
     _say("[V=1]")
     lists_h = _random_lists(w, np.random.default_rng(3))
     og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, v_override=lambda v: np.full_like(v, 0x3F80))
-    # O = sum(bf16(p)) / sum(p): within one bf16 step of 1 (1 - 2^-8 .. 1 + 2^-7)
-    assert (og >= 1.0 - 2.0 ** -8).all() and (og <= 1.0 + 2.0 ** -7).all()
-    assert (og == 1.0).mean() > 0.5
+    # the row sum is over the same bf16 P that multiplies V, so the weights sum to one
+    assert (og == 1.0).all()
 
 
 def test_zero_queries_average_selected_values(gpu_lib):
@@ -331,8 +331,10 @@ def test_split_agrees_with_single_pass(gpu_lib):
     o1, l1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, split=True)
     o2, l2 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, split=False)
     torch.cuda.synchronize()
-    assert (o1.float() - o2.float()).abs().max().item() <= 1e-2
-    assert (l1 - l2).abs().max().item() <= 1e-4
+    # P is rounded relative to each range's own running max, so the two paths
+    # round differently; each is within the bf16-P bounds of the exact result
+    assert (o1.float() - o2.float()).abs().max().item() <= O_MAX_ABS
+    assert (l1 - l2).abs().max().item() <= LSE_ABS
 
 
 def test_deterministic(gpu_lib):
