@@ -60,7 +60,8 @@ struct AttnCfg {
   static constexpr int DS = D / 16;           // MFMA k-steps over D
   static constexpr int DT = D / 32;           // 32-row d tiles of O^T
   static constexpr int KLD = D + 8;           // K row pitch (bf16): consecutive rows 4 banks apart
-  static constexpr int VLD = D + 16;          // V row pitch (bf16): consecutive rows 8 banks apart
+  static constexpr int VLD = D + 32;          // V row pitch (bf16): consecutive rows 16 banks apart, so the
+                                              // two 16-lane groups of a transpose read fill disjoint banks
   static constexpr int K_ELEMS = BLK * KLD;
   static constexpr int V_ELEMS = BLK * VLD;
   static constexpr int STAGE = K_ELEMS + V_ELEMS;
@@ -226,10 +227,8 @@ void attn_fwd_kernel(AttnArgs a) {
   uint32_t voff[C::CH];
 #pragma unroll
   for (int p = 0; p < C::CH; ++p) voff[p] = (uint32_t)((row0 + p * C::ROWS_PER_PASS) * D + col8) * 2u;
-  auto tile_bytes = [&](int blk) -> uint32_t {
-    const int64_t left = (a.lk - (int64_t)blk * BLK) * D * 2;
-    return left < TILE_BYTES ? (uint32_t)left : TILE_BYTES;
-  };
+  const uint32_t last_bytes = (uint32_t)(a.lk - (int64_t)(a.n_k - 1) * BLK) * (D * 2);
+  auto tile_bytes = [&](int blk) -> uint32_t { return blk == a.n_k - 1 ? last_bytes : TILE_BYTES; };
   uint4 kreg[C::CH], vreg[C::CH];
   auto load_k = [&](int blk) {
     const __amdgpu_buffer_rsrc_t rs = make_rsrc(kbase + (int64_t)blk * BLK * D, tile_bytes(blk));
@@ -275,8 +274,45 @@ void attn_fwd_kernel(AttnArgs a) {
     }
   };
 
+  const float sl2 = a.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // keys >= Lk of a partial last block get -inf scores
+  auto mask_tail = [&](f32x16* acc, int blk) {
+    const int64_t key0 = (int64_t)blk * BLK;
+    if (key0 + BLK > a.lk) {
+#pragma unroll
+      for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = kh * C::KH + kt * 32 + 8 * (e / 4) + 4 * hh + (e % 4);
+          if (key0 + key >= a.lk) acc[kt][e] = -INFINITY;
+        }
+    }
+  };
+  // running max for a new score tile, with lazy rescaling: O and l are only
+  // rescaled when a query's maximum grows by more than 2^8
+  auto update_max = [&](const f32x16* acc) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[kt][e]);
+    mx = half_swap_max(mx) * sl2;  // the tile's max logit (log2 domain) for the lane's query
+    if (__any(mx > m_run + 8.0f)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc_o[t][e] *= alpha;
+      m_run = m_new;
+    }
+  };
+
   // ---- prologue: K of tiles 0 and 1 and V of tile 0 staged, K of tile 2 and
-  // V of tile 1 in flight, S of tile 0 computed
+  // V of tile 1 in flight, S of tile 0 computed and its max applied
   int b0 = fetch_next();
   int b1 = fetch_next();
   int b2 = fetch_next();
@@ -294,60 +330,47 @@ void attn_fwd_kernel(AttnArgs a) {
   }
   if (b2 >= 0) load_k(b2);
   __syncthreads();
-  if (b0 >= 0) scores(0, acc_s);
+  if (b0 >= 0) {
+    scores(0, acc_s);
+    mask_tail(acc_s, b0);
+    update_max(acc_s);
+  }
   __syncthreads();  // K buffer 0 is rewritten in the first step
 
-  const float sl2 = a.scale_log2;
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-
-  // one step: softmax and O += P V of tile t (block b0) while the scores of
-  // tile t+1 (block b1) run on the matrix cores
+  // One step: P and O += P V of tile t (block b0) while the scores of tile t+1
+  // (block b1) run on the matrix cores.  The compute block has no branch, and
+  // sched_group_barrier interleaves each score MFMA with the exponentials of
+  // the current tile and each P V MFMA with a row-sum update, so the VALU work
+  // hides under the matrix-core work of the same wave.
   auto step = [&](auto parity) {
     constexpr int P = decltype(parity)::value;
     f32x16 acc_n[C::KT];
-    if (b1 >= 0) scores(1 - P, acc_n);
+    const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
 
-    // keys >= Lk (only in a partial last block) are masked
-    const int64_t key0 = (int64_t)b0 * BLK;
-    if (key0 + BLK > a.lk) {
-#pragma unroll
-      for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = kh * C::KH + kt * 32 + 8 * (e / 4) + 4 * hh + (e % 4);
-          if (key0 + key >= a.lk) acc_s[kt][e] = -INFINITY;
-        }
-    }
-
-    // online softmax with lazy rescaling
-    float mx = -INFINITY;
+    // K of tile t+1 (buffer 1-P; stale but harmless when there is no such tile)
+    uint4 kf[C::KT][C::DS];
+    const uint16_t* ks = k_rd + (1 - P) * C::K_ELEMS;
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc_s[kt][e]);
-    mx = half_swap_max(mx) * sl2;  // this step's max logit (log2 domain) for the lane's query
-    if (__any(mx > m_run + 8.0f)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc_o[t][e] *= alpha;
-      m_run = m_new;
-    }
-    const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
+      for (int s = 0; s < C::DS; ++s) kf[kt][s] = *reinterpret_cast<const uint4*>(ks + kt * 32 * C::KLD + 16 * s);
+
     uint32_t pk[C::KT][8];  // bf16 pairs of P^T, per 32-key sub-tile
 #pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt)
+    for (int kt = 0; kt < C::KT; ++kt) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc_n[kt][e] = 0.f;
+#pragma unroll
+      for (int s = 0; s < C::DS; ++s)
+        acc_n[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kt][s]), qf[s], acc_n[kt],
+                                                            0, 0, 0);
 #pragma unroll
       for (int e = 0; e < 16; e += 2) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
-        const bf16x2 pp = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
-        pk[kt][e / 2] = __builtin_bit_cast(uint32_t, pp);
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l_run, false);
+        pk[kt][e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
       }
+    }
 
     // O^T += V^T P^T over 16-key k-steps (V tile of block b0 in buffer P)
     const uint16_t* vs = v_rd + P * C::V_ELEMS;
@@ -373,7 +396,34 @@ void attn_fwd_kernel(AttnArgs a) {
           const s16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
           acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, acc_o[t], 0, 0, 0);
         }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][4 * half + i]), ones, l_run,
+                                                  false);
       }
+    if constexpr (C::KT == 1 && C::DS == 8 && C::DT == 4) {
+      // K reads first; then 8 x (score MFMA + 5 VALU of the exponentials + 2 V
+      // transpose reads, so the V operands land while the exponentials run);
+      // then 8 x (P V MFMA + 1 row-sum VALU)
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+      }
+    }
+
+    // scores of tile t+1: tail mask and running max (rescales O if needed)
+    if (b1 >= 0) {
+      mask_tail(acc_n, b1);
+      update_max(acc_n);
+    }
 
     // stage K of t+2 and V of t+1, start the loads of K of t+3 and V of t+2
     if (b2 >= 0) store_k(P);
