@@ -9,17 +9,22 @@ seeded synthetic bf16 tensors already resident in HBM.
 
 Prints ONE JSON line.  `value` is effective TFLOP/s of the step: FLOPs executed
 on the selected blocks (4 * 64 * 64 * D per (query block, listed key block))
-divided by the step time.  `roofline` reports the sparse forward kernel against
-the bf16 MFMA peak, timed with HIP events on the stream it runs on.
-`cpu_baseline` times the float64 CPU oracle on a bounded sample of the same
-workload and scales it to the whole call.
+divided by the step time.  `roofline` reports the sparse forward call against
+the bf16 MFMA peak, timed with HIP events on the stream it runs on; `traffic`
+comes from the committed rocprofv3 counter summary when it was taken on the
+current kernel source.  Also reported: the in-house dense forward on the same
+shape, the density sweep (per-head budgets around 10 / 25 / 50%), the
+five-scale clip pyramid, and the float64 CPU oracle timed on a bounded sample
+(`cpu_baseline`).
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import platform
+import re
 import sys
 import time
 
@@ -31,7 +36,8 @@ if ROOT not in sys.path:
 
 METRIC = "ms and effective TFLOP/s per sparse attention call at 72k-query 720p scale"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
-PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_sparse_720p_hbm.md")
+ATTN_SOURCE = os.path.join(ROOT, "paper_2608_10519_amd", "csrc", "attn_fwd.hip")
 
 
 def log(msg: str) -> None:
@@ -39,10 +45,25 @@ def log(msg: str) -> None:
 
 
 def executed_flops(num_blocks: np.ndarray, lq: int, lk: int, block: int, d: int) -> float:
-    """Sum over (b, h, i) of 4 * rows_i * keys(A_i) * D, with full blocks (the
-    720p shapes are multiples of 64)."""
+    """Sum over (b, h, i) of 4 * rows_i * keys(A_i) * D with full blocks (the
+    shapes measured here are multiples of the block size)."""
     assert lq % block == 0 and lk % block == 0
     return float(num_blocks.astype(np.float64).sum()) * 4.0 * block * block * d
+
+
+def traffic_from_profile() -> dict | None:
+    """HBM bytes per launch of the sparse attention kernel from the committed
+    counter summary, if it was measured on the current kernel source."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    text = open(TRAFFIC_SUMMARY).read()
+    src = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()
+    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    m_f = re.search(r"fetch_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    m_w = re.search(r"write_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not (m_sha and m_f and m_w) or m_sha.group(1) != src:
+        return None
+    return {"fetch": float(m_f.group(1)), "write": float(m_w.group(1))}
 
 
 def cpu_baseline(w, qb, kb, vb, keep, total_flops: float, lists_gpu) -> dict:
@@ -63,7 +84,7 @@ def cpu_baseline(w, qb, kb, vb, keep, total_flops: float, lists_gpu) -> dict:
     t0 = time.perf_counter()
     lists, _, _, _ = O.select(q, k, w.block, w.density, keep)
     t_sel = time.perf_counter() - t0
-    sample = [0, n_q // 3, (2 * n_q) // 3, n_q - 1, 17, 500, 900, 1100]
+    sample = sorted(set(np.linspace(0, n_q - 1, 48).astype(int).tolist()))
     t0 = time.perf_counter()
     for i in sample:
         rows = slice(i * w.block, (i + 1) * w.block)
@@ -78,10 +99,72 @@ def cpu_baseline(w, qb, kb, vb, keep, total_flops: float, lists_gpu) -> dict:
         "cores": int(threads),
         "kind": "oracle",
         "sample": (f"head 0 of 24: full selector ({n_q} rows, {t_sel:.1f} s) + attention of {len(sample)} "
-                   f"query blocks ({t_att:.2f} s each), scaled to 24 heads x {n_q} blocks"),
+                   f"evenly spaced query blocks ({t_att:.3f} s each), scaled to 24 heads x {n_q} blocks"),
         "cpu": platform.processor() or platform.machine(),
         "lists_equal_gpu_head0": agree,
     }
+
+
+class Runner:
+    """Device buffers and timed C-ABI calls for one workload shape."""
+
+    def __init__(self, S, torch, w, qb, kb, vb, budget):
+        self.S, self.torch, self.w = S, torch, w
+        dev = torch.device("cuda:0")
+        up = lambda bits: torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+        self.q, self.k, self.v = up(qb), up(kb), up(vb)
+        from synthetic import keep_ranges
+
+        self.keep = keep_ranges(w)
+        self.budget = budget
+        B, H, Lq, D = self.q.shape
+        Lk = self.k.shape[2]
+        self.shape = (B, H, Lq, Lk, D)
+        self.stride = S.sparstar_kv_stride(H, Lk, w.block, budget, self.keep)
+        n_q = -(-Lq // w.block)
+        self.num = torch.empty((B, H, n_q), dtype=torch.int32, device=dev)
+        self.idx = torch.empty((B, H, n_q, self.stride), dtype=torch.int32, device=dev)
+        self.ws = torch.empty(S.sparstar_score_workspace_bytes(B, H, Lq, Lk, D, w.block), dtype=torch.uint8,
+                              device=dev)
+        self.aws = torch.empty(max(1, S.sparstar_attn_workspace_bytes(B, H, Lq, Lk, D, w.block)), dtype=torch.uint8,
+                               device=dev)
+        self.o = torch.empty_like(self.q)
+        self.lse = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+
+    def ev(self):
+        return self.torch.cuda.Event(enable_timing=True)
+
+    def score(self):
+        self.S.sparstar_score_blocks(self.q, self.k, self.w.block, self.budget, self.keep, kv_stride=self.stride,
+                                     workspace=self.ws, out=(self.num, self.idx))
+
+    def sparse(self):
+        self.S.sparstar_sparse_attn_fwd(self.q, self.k, self.v, self.num, self.idx, self.w.block, out=self.o,
+                                        lse=self.lse, workspace=self.aws)
+
+    def dense(self):
+        self.S.sparstar_dense_attn_fwd(self.q, self.k, self.v, self.w.block, out=self.o, lse=self.lse,
+                                       workspace=self.aws)
+
+    def timed(self, fn, reps: int, warm: int = 1) -> list[float]:
+        for _ in range(warm):
+            fn()
+        self.torch.cuda.synchronize()
+        marks = [(self.ev(), self.ev()) for _ in range(reps)]
+        for a, b in marks:
+            a.record()
+            fn()
+            b.record()
+        self.torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in marks]
+
+    def flops(self) -> float:
+        B, H, Lq, Lk, D = self.shape
+        return executed_flops(self.num.cpu().numpy(), Lq, Lk, self.w.block, D)
+
+    def dense_flops(self) -> float:
+        B, H, Lq, Lk, D = self.shape
+        return 4.0 * B * H * Lq * Lk * D
 
 
 def main() -> int:
@@ -92,6 +175,8 @@ def main() -> int:
     ap.add_argument("--density", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-pyramid", action="store_true")
     ap.add_argument("--gen-workers", type=int, default=None,
                     help="input-generation processes (1 = in-process; use 1 under a profiler)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -114,12 +199,16 @@ def main() -> int:
         print(json.dumps({"copy_calibration": {"read_bytes": 4 * n, "write_bytes": 4 * n, "launches": 3}}))
         return 0
 
-    from synthetic import P720, generate, keep_ranges
+    from synthetic import P720, SWEEP, SWEEP_DENSITIES, generate, head_densities, pyramid_scales
 
+    # all inputs are generated before the GPU is touched
     w = P720 if args.density is None else P720.with_(density=args.density)
     log(f"generating {w.name}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk} rho={w.density}")
     t0 = time.perf_counter()
-    qb, kb, vb = generate(w, workers=args.gen_workers)
+    data = generate(w, workers=args.gen_workers)
+    sweep_data = None if args.no_sweep else generate(SWEEP, workers=args.gen_workers)
+    pyr = [] if args.no_pyramid else [(pw, sparse, generate(pw, workers=args.gen_workers))
+                                      for pw, sparse in pyramid_scales()]
     log(f"generated in {time.perf_counter() - t0:.1f} s")
 
     import torch
@@ -127,61 +216,38 @@ def main() -> int:
     from paper_2608_10519_amd import sparstar as S
 
     S.load()
-    dev = torch.device("cuda:0")
-
-    def up(bits):
-        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
-
-    q, k, v = up(qb), up(kb), up(vb)
-    keep = keep_ranges(w)
-    B, H, Lq, D = q.shape
-    Lk = k.shape[2]
-    stride = S.sparstar_kv_stride(H, Lk, w.block, w.density, keep)
-    n_q = Lq // w.block
-    num = torch.empty((B, H, n_q), dtype=torch.int32, device=dev)
-    idx = torch.empty((B, H, n_q, stride), dtype=torch.int32, device=dev)
-    ws = torch.empty(S.sparstar_score_workspace_bytes(B, H, Lq, Lk, D, w.block), dtype=torch.uint8, device=dev)
-    o = torch.empty_like(q)
-    lse = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
-    aws = torch.empty(max(1, S.sparstar_attn_workspace_bytes(B, H, Lq, Lk, D, w.block)), dtype=torch.uint8,
-                      device=dev)
-    torch.cuda.synchronize()
-
-    ev = lambda: torch.cuda.Event(enable_timing=True)
-
-    def step(record=None):
-        if record is not None:
-            record[0].record()
-        S.sparstar_score_blocks(q, k, w.block, w.density, keep, kv_stride=stride, workspace=ws, out=(num, idx))
-        if record is not None:
-            record[1].record()
-        S.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, out=o, lse=lse, workspace=aws)
-        if record is not None:
-            record[2].record()
+    r = Runner(S, torch, w, *data, w.density)
+    B, H, Lq, Lk, D = r.shape
 
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
-        step()
+        r.score()
+        r.sparse()
     torch.cuda.synchronize()
 
     log(f"timing {args.steps} steps")
-    marks = [(ev(), ev(), ev()) for _ in range(args.steps)]
+    marks = [(r.ev(), r.ev(), r.ev()) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for m in marks:
-        step(m)
+        m[0].record()
+        r.score()
+        m[1].record()
+        r.sparse()
+        m[2].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     sel_ms = [m[0].elapsed_time(m[1]) for m in marks]
     att_ms = [m[1].elapsed_time(m[2]) for m in marks]
     ms_step = wall * 1e3 / args.steps
 
-    counts = num.cpu().numpy()
-    flops = executed_flops(counts, Lq, Lk, w.block, D)
+    counts = r.num.cpu().numpy()
+    flops = r.flops()
     att_avg = float(np.mean(att_ms))
     achieved = flops / (att_avg * 1e-3) / 1e12
     log(f"step {ms_step:.3f} ms  selector {np.mean(sel_ms):.3f} ms  sparse fwd {att_avg:.3f} ms  "
         f"({achieved:.1f} TFLOP/s)")
+    tr = traffic_from_profile()
 
     out = {
         "metric": METRIC,
@@ -210,40 +276,73 @@ def main() -> int:
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "sparse forward call: attn_fwd_kernel<128,64,sparse,split> + attn_merge_kernel",
+            "kernel": "sparse forward call (attn_fwd_kernel<128,64,sparse,split> + attn_merge_kernel)",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": None if tr is None else tr["fetch"] + tr["write"],
         },
     }
+    if tr is not None:
+        out["roofline"]["traffic_detail_bytes"] = tr
 
+    dense_ms = None
     if not args.no_dense:
         log("dense comparison")
-        e0, e1 = ev(), ev()
-        S.sparstar_dense_attn_fwd(q, k, v, w.block, out=o, lse=lse, workspace=aws)  # warm
-        torch.cuda.synchronize()
-        e0.record()
-        S.sparstar_dense_attn_fwd(q, k, v, w.block, out=o, lse=lse, workspace=aws)
-        e1.record()
-        torch.cuda.synchronize()
-        dense_ms = e0.elapsed_time(e1)
-        dense_flops = 4.0 * B * H * Lq * Lk * D
+        dense_ms = float(np.mean(r.timed(r.dense, 2)))
         out["dense"] = {
             "ms": dense_ms,
-            "tflops": dense_flops / (dense_ms * 1e-3) / 1e12,
+            "tflops": r.dense_flops() / (dense_ms * 1e-3) / 1e12,
             "speedup_sparse_step": dense_ms / ms_step,
             "speedup_sparse_fwd_only": dense_ms / att_avg,
         }
         log(f"dense {dense_ms:.2f} ms -> speedup {dense_ms / ms_step:.2f}x (step), {dense_ms / att_avg:.2f}x (fwd)")
 
+    if sweep_data is not None:
+        log("density sweep (per-head budgets U[0.5, 1.5] x rho)")
+        rows = []
+        for rho in SWEEP_DENSITIES:
+            budgets = head_densities(SWEEP, rho).tolist()
+            rs = Runner(S, torch, SWEEP, *sweep_data, budgets)
+            sc = float(np.mean(rs.timed(rs.score, 3)))
+            sp = float(np.mean(rs.timed(rs.sparse, 3)))
+            fl = rs.flops()
+            row = {"density": rho, "score_ms": sc, "sparse_fwd_ms": sp, "step_ms": sc + sp,
+                   "executed_tflop": fl / 1e12, "tflops": fl / (sp * 1e-3) / 1e12,
+                   "scoring_overhead": sc / sp}
+            if dense_ms is not None:
+                row["speedup_vs_dense_step"] = dense_ms / (sc + sp)
+                row["speedup_vs_dense_fwd"] = dense_ms / sp
+            rows.append(row)
+            log(f"  rho={rho}: score {sc:.2f} ms, sparse {sp:.2f} ms ({row['tflops']:.0f} TFLOP/s)")
+            del rs
+        out["sweep"] = rows
+
+    if pyr:
+        log("clip pyramid (dense scales 1-3, fresh selection + sparse scales 4-5)")
+        scales, total = [], 0.0
+        for pw, sparse, pdata in pyr:
+            rp = Runner(S, torch, pw, *pdata, pw.density)
+            if sparse:
+                ms = float(np.mean(rp.timed(lambda: (rp.score(), rp.sparse()), 2)))
+                fl = rp.flops()
+            else:
+                ms = float(np.mean(rp.timed(rp.dense, 2)))
+                fl = rp.dense_flops()
+            total += ms
+            scales.append({"lq": pw.lq, "lk": pw.lk, "mode": "sparse" if sparse else "dense", "ms": ms,
+                           "executed_tflop": fl / 1e12})
+            log(f"  Lq={pw.lq}: {'sparse' if sparse else 'dense'} {ms:.2f} ms")
+            del rp
+        out["pyramid"] = {"total_ms": total, "scales": scales}
+
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle on a bounded sample)")
         num_h0 = counts[0, 0]
-        idx_h0 = idx[0, 0].cpu().numpy()
-        lists_h0 = [idx_h0[i, : num_h0[i]].tolist() for i in range(n_q)]
-        out["cpu_baseline"] = cpu_baseline(w, qb, kb, vb, keep, flops, lists_h0)
+        idx_h0 = r.idx[0, 0].cpu().numpy()
+        lists_h0 = [idx_h0[i, : num_h0[i]].tolist() for i in range(Lq // w.block)]
+        out["cpu_baseline"] = cpu_baseline(w, *data, r.keep, flops, lists_h0)
         log(f"cpu baseline {out['cpu_baseline']['value']:.4f} TFLOP/s")
 
     print(json.dumps(out), flush=True)

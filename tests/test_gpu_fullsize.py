@@ -1,0 +1,91 @@
+"""GPU parity at the full workload sizes, on sampled outputs the oracle can
+compute one by one.
+
+All 24 heads run through the C ABI in the launch configuration the benchmark
+times (key-range split with a workspace); the float64 oracle then recomputes
+the selector of sampled heads completely (every row checked under the gap
+rule) and the forward of sampled query blocks (first, last and interior ones).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+from synthetic import MID, P720, SWEEP, bf16_to_f64, generate, head_densities, keep_ranges
+from tests.helpers import check_gap_rule, check_output, to_dev
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _run_full(lib, w, budget):
+    import torch
+
+    _say(f"[full] {w.name}: generating H={w.heads} Lq={w.lq} Lk={w.lk}")
+    qb, kb, vb = generate(w, workers=1)
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    keep = keep_ranges(w)
+    _say(f"[full] {w.name}: selector + sparse forward on the GPU")
+    num, idx = lib.sparstar_score_blocks(q, k, w.block, budget, keep)
+    o, lse = lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
+    torch.cuda.synchronize()
+    return (qb, kb, vb), keep, num.cpu().numpy(), idx.cpu().numpy(), o.float().cpu().numpy(), lse.cpu().numpy()
+
+
+def _check_heads(w, data, keep, num, idx, o, lse, heads, qblocks, budgets):
+    qb, kb, vb = data
+    n_q = -(-w.lq // w.block)
+    for h in heads:
+        qh, kh, vh = bf16_to_f64(qb[0, h]), bf16_to_f64(kb[0, h]), bf16_to_f64(vb[0, h])
+        rho = float(budgets[h])
+        _say(f"[full] {w.name}: oracle selector head {h} (rho={rho:.4f})")
+        lists_ref, s_ref, kk, keep_set = O.select(qh, kh, w.block, rho, keep)
+        sel = O.selectable_blocks(keep_set, w.lk, w.block)
+        stats = {"exact": 0, "tolerant": 0}
+        gpu_lists = []
+        for i in range(n_q):
+            row = idx[0, h, i, : num[0, h, i]].tolist()
+            stats[check_gap_rule(row, s_ref[i], keep_set, sel, kk)] += 1
+            gpu_lists.append(row)
+        _say(f"[full] {w.name}: head {h} rows {stats}")
+        for i in qblocks:
+            rows = slice(i * w.block, min((i + 1) * w.block, w.lq))
+            o_ref, l_ref = O.sparse_attention(qh[rows], kh, vh, [gpu_lists[i]], w.block)
+            check_output(o[0, h, rows][None].astype(np.float64), o_ref[None], lse[0, h, rows][None].astype(np.float64),
+                         l_ref[None], what=f"{w.name} head {h} block {i}")
+
+
+def test_mid_scale_parity(gpu_lib):
+    w = MID
+    data, keep, num, idx, o, lse = _run_full(gpu_lib, w, w.density)
+    n_q = -(-w.lq // w.block)
+    _check_heads(w, data, keep, num, idx, o, lse, heads=[0, 13, 23], qblocks=[0, 1, 90, n_q - 1],
+                 budgets=np.full(w.heads, w.density))
+
+
+def test_720p_final_scale_parity(gpu_lib):
+    w = P720
+    data, keep, num, idx, o, lse = _run_full(gpu_lib, w, w.density)
+    n_q = -(-w.lq // w.block)
+    assert (num == 8 + 563).all()
+    _check_heads(w, data, keep, num, idx, o, lse, heads=[0, 17], qblocks=[0, 561, n_q - 1],
+                 budgets=np.full(w.heads, w.density))
+
+
+def test_720p_per_head_budget_sweep_parity(gpu_lib):
+    """The density sweep's per-head budgets (U[0.5, 1.5] x 10%)."""
+    w = SWEEP
+    budgets = head_densities(w, 0.10)
+    data, keep, num, idx, o, lse = _run_full(gpu_lib, w, budgets.tolist())
+    n_sel = -(-w.lk // w.block) - 8
+    for h in range(w.heads):
+        assert (num[0, h] == 8 + O.budget_k(float(budgets[h]), n_sel)).all()
+    _check_heads(w, data, keep, num, idx, o, lse, heads=[int(np.argmax(budgets))], qblocks=[3, 1000],
+                 budgets=budgets)
