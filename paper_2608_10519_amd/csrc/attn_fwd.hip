@@ -1,19 +1,20 @@
 // Block-sparse attention forward (Eq. 7, Section 5.3) and its dense variant.
 //
 // Work decomposition.  One work-group per (batch*head, query block of BLK
-// rows), launched head-major so that all eight XCDs work on the same head at a
-// time and that head's K/V (74 MB at the 720p shape) stays resident in the
-// 256 MB last-level cache.  The work-group has 2 * BLK/32 wavefronts: wave w
-// owns the 32-row query slice (w % (BLK/32)) and the key half (w / (BLK/32)) of
-// every key block, so each wave touches only half of each K and V tile and two
-// waves per SIMD stay resident (<= 256 VGPRs each).
+// rows, key range), launched so that the eight XCDs stream disjoint key ranges
+// of the same head (see the work-item decode below).  The work-group has
+// 2 * BLK/32 wavefronts: wave w owns the 32-row query slice (w % (BLK/32)) and
+// the key half (w / (BLK/32)) of every key block, so each wave touches only
+// half of each K and V tile and two waves per SIMD stay resident (<= 256 VGPRs
+// each).
 //
 // Per key block of the query block's ascending list:
-//   * K and V tiles (BLK x D each) are copied row-major into LDS with coalesced
-//     16-byte loads and stores (row pitches padded so that the operand reads
-//     below are bank-conflict-free).  LDS is double-buffered: the tile of step
-//     t+1 is written while step t computes (one barrier per step) and the global
-//     loads of step t+2 are in flight during the whole step;
+//   * K and V tiles (BLK x D each) go from global memory straight into LDS
+//     (buffer_load ... lds, 1 KB per wave instruction, coalesced), with no
+//     VGPR staging.  LDS holds a ring of three K tiles and two V tiles: the K
+//     tile is needed one step before the V tile of the same block, and the
+//     loads of K(t+3) and V(t+1) are issued at the start of step t, so one
+//     barrier per step suffices;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (fp32 accumulate).  The
 //     transpose leaves each lane holding 16 keys of ONE query column -- exactly
 //     the B-operand layout P^T needs -- so the softmax state is lane-local up to
@@ -59,17 +60,34 @@ struct AttnCfg {
   static constexpr int KT = KH / 32;          // 32-key sub-tiles per wave and step
   static constexpr int DS = D / 16;           // MFMA k-steps over D
   static constexpr int DT = D / 32;           // 32-row d tiles of O^T
-  static constexpr int KLD = D + 8;           // K row pitch (bf16): consecutive rows 4 banks apart
-  static constexpr int VLD = D + 32;          // V row pitch (bf16): consecutive rows 16 banks apart, so the
-                                              // two 16-lane groups of a transpose read fill disjoint banks
-  static constexpr int K_ELEMS = BLK * KLD;
-  static constexpr int V_ELEMS = BLK * VLD;
-  static constexpr int STAGE = K_ELEMS + V_ELEMS;
-  static constexpr int CPR = D / 8;                 // 16-byte chunks per row
-  static constexpr int CH = BLK * CPR / NT;         // chunks per thread, for each of K and V
-  static constexpr int ROWS_PER_PASS = NT / CPR;    // rows covered by one chunk pass
-  static_assert(CH * NT == BLK * CPR, "tile split");
+  static constexpr int RB = D * 2;            // bytes per K/V row
+  static constexpr int CPR = D / 8;           // 16-byte chunks per row
+  static constexpr int RPB = 256 / RB;        // rows per 256 bytes (one pass over the 64 LDS banks)
+  static constexpr int TILE = BLK * D;        // elements per K or V tile
+  static constexpr int TILE_BYTES = TILE * 2;
+  static constexpr int RPD = 1024 / RB;       // rows per direct-to-LDS wave load (64 lanes x 16 B)
+  static constexpr int DPW = TILE_BYTES / 1024 / NW;  // direct loads per wave and tile
+  static_assert(DPW * NW * 1024 == TILE_BYTES, "tile split over the waves");
+  static_assert(KT * 32 * 2 == BLK, "key halves");
 };
+
+// LDS tiles are stored unpadded (a direct-to-LDS load writes 1 KB contiguous
+// per wave), with the 16-byte chunks of each row XOR-permuted so that both
+// operand reads are free of bank conflicts:
+//   K (ds_read_b128, 16 lanes per pass: 16 consecutive rows, one chunk):
+//     physical chunk = c ^ (r / RPB mod CPR)
+//   V (ds_read_b64_tr_b16, 32 lanes per pass: 4 consecutive rows x 4 chunks):
+//     physical chunk = c ^ ((r / RPB mod 4) * 4 mod CPR)
+template <int D, int BLK>
+__device__ __forceinline__ int k_swz(int r) {
+  using C = AttnCfg<D, BLK>;
+  return (r / C::RPB) % C::CPR;
+}
+template <int D, int BLK>
+__device__ __forceinline__ int v_swz(int r) {
+  using C = AttnCfg<D, BLK>;
+  return (((r / C::RPB) & 3) << 2) & (C::CPR - 1);
+}
 
 __device__ __forceinline__ float half_swap_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -95,19 +113,54 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+// Buffer descriptor as four dwords (raw buffer, stride 0, `bytes` records):
+// the form the inline-asm direct-to-LDS load takes.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 raw_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)p);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(p >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;
+  return r;
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)p);
+}
+
+// One wave-wide direct-to-LDS load: lane l copies 16 bytes from buffer offset
+// voff to LDS byte m0 + 16 l.  Written as inline assembly so that the compiler
+// does not order every later LDS read behind it; each caller waits for these
+// loads explicitly (vmcnt) before a barrier makes the tile visible.
+__device__ __forceinline__ void dma16(uint32_t m0, uint32_t voff, i32x4 rsrc) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds"
+      :
+      : "s"(m0), "v"(voff), "s"(rsrc)
+      : "memory", "m0");
+}
+
+// s_waitcnt with only the vector-memory counter constrained (<= n outstanding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 template <int D, int BLK, bool DENSE, bool SPLIT>
 __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a) {
   using C = AttnCfg<D, BLK>;
-  // K double buffer, then V double buffer.  Step t reads K of tile t+1 (for the
-  // scores one step ahead) and V of tile t, while K of t+2 and V of t+1 are
-  // written into the other halves.
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::K_ELEMS + 2 * C::V_ELEMS];
-  __shared__ int list_pos[2];
+  // Ring of three K tiles and two V tiles.  Step t reads K of tile t+1 (the
+  // scores one step ahead) and V of tile t; at its start it issues the
+  // direct-to-LDS loads of V of tile t+1 and K of tile t+3 into the slots that
+  // the previous step released.  K(j) lives in slot j mod 3, V(j) in j mod 2.
+  __shared__ __attribute__((aligned(1024))) uint16_t ks0[C::TILE], ks1[C::TILE], ks2[C::TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t vs0[C::TILE], vs1[C::TILE];
 
   // Work item.  Work-groups are dispatched round-robin over the eight XCDs, so
   // with the key-range split the work-group id decodes as
@@ -128,71 +181,64 @@ void attn_fwd_kernel(AttnArgs a) {
   const int blk_lo = SPLIT ? (int)((int64_t)split * a.n_k / kSplits) : 0;
   const int blk_hi = SPLIT ? (int)((int64_t)(split + 1) * a.n_k / kSplits) : a.n_k;
 
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const int l32 = lane % 32, hh = lane / 32;
   const int qs = wave % C::NQS;   // query slice
   const int kh = wave / C::NQS;   // key half
 
-  // ---- list positions [pos_lo, pos_hi) that may hold blocks of [blk_lo, blk_hi)
-  int pos_lo, pos_hi;
+  // ---- the list positions [pos_lo, pos_lo + cnt) that hold the blocks of
+  // [blk_lo, blk_hi): an ascending list has them after the entries < blk_lo and
+  // before the entries >= blk_hi (every wave counts them itself)
+  int pos_lo, cnt;
   const int32_t* list = nullptr;
   if constexpr (DENSE) {
     pos_lo = blk_lo;
-    pos_hi = blk_hi;
+    cnt = blk_hi - blk_lo;
   } else {
     const int64_t r = bh * a.n_q + qb;
     int nblk = a.kv_num_blocks[r];
     nblk = nblk < 0 ? 0 : (nblk > a.stride ? a.stride : nblk);
     list = a.kv_indices + r * a.stride;
-    if constexpr (SPLIT) {
-      // an ascending list: the range starts after the entries < blk_lo and ends
-      // after the entries < blk_hi
-      if (tid < 2) list_pos[tid] = 0;
-      __syncthreads();
-      int c_lo = 0, c_hi = 0;
-      for (int i = tid; i < nblk; i += C::NT) {
-        const int j = list[i];
-        c_lo += j < blk_lo;
-        c_hi += j < blk_hi;
-      }
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        c_lo += __shfl_xor(c_lo, off, 64);
-        c_hi += __shfl_xor(c_hi, off, 64);
-      }
-      if (lane == 0) {
-        atomicAdd(&list_pos[0], c_lo);
-        atomicAdd(&list_pos[1], c_hi);
-      }
-      __syncthreads();
-      pos_lo = list_pos[0];
-      pos_hi = list_pos[1];
-    } else {
-      pos_lo = 0;
-      pos_hi = nblk;
+    int c_lo = 0, c_hi = 0;
+    for (int i = lane; i < nblk; i += 64) {
+      const int j = list[i];
+      c_lo += j < blk_lo;
+      c_hi += j < blk_hi;
     }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      c_lo += __shfl_xor(c_lo, off, 64);
+      c_hi += __shfl_xor(c_hi, off, 64);
+    }
+    pos_lo = __builtin_amdgcn_readfirstlane(c_lo);
+    cnt = __builtin_amdgcn_readfirstlane(c_hi) - pos_lo;
   }
 
-  // ---- block cursor: the next list entry is prefetched one call ahead with a
-  // vector-memory load, so its latency hides behind a whole step
-  int cur_pos = pos_lo;
-  // (the range check covers the vector offset, so the position goes there:
-  // reading one past the end returns 0 instead of touching memory)
-  const __amdgpu_buffer_rsrc_t list_rs = make_rsrc(list, DENSE ? 0u : (uint32_t)pos_hi * 4u);
-  uint32_t pf = 0;
-  if constexpr (!DENSE) pf = __builtin_amdgcn_raw_buffer_load_b32(list_rs, (uint32_t)cur_pos * 4u, 0u, 0);
-  // next block of [blk_lo, blk_hi) in list order, or -1
-  auto fetch_next = [&]() -> int {
+  // ---- block of list position pos_lo + j.  The entries are held 64 at a time
+  // in a VGPR (lane i: entry lbase + i) and picked out with v_readlane, so the
+  // loop issues no memory load of its own except one batch load per 64 tiles.
+  // j >= cnt, and an entry outside [blk_lo, blk_hi) -- only possible in a list
+  // that is not ascending --, give -1: a tile that is loaded as zeros and fully
+  // masked.
+  int lreg = -1, lbase = 0;
+  auto load_batch = [&](int base) {
+    lbase = base;
+    if constexpr (!DENSE) {
+      lreg = base + lane < cnt ? list[pos_lo + base + lane] : -1;
+      // consume the load here, so that its wait stays on this rare path and is
+      // not merged into the common path of the loop
+      asm volatile("; list batch %0" ::"v"(lreg));
+    }
+  };
+  auto fetch = [&](int j) -> int {
+    if (j >= cnt) return -1;
     if constexpr (DENSE) {
-      return cur_pos < pos_hi ? cur_pos++ : -1;
+      return blk_lo + j;
     } else {
-      while (cur_pos < pos_hi) {
-        const int j = __builtin_amdgcn_readfirstlane((int)pf);
-        ++cur_pos;
-        pf = __builtin_amdgcn_raw_buffer_load_b32(list_rs, (uint32_t)cur_pos * 4u, 0u, 0);
-        if (j >= blk_lo && j < blk_hi) return j;
-      }
-      return -1;
+      if (j >= lbase + 64) load_batch(lbase + 64);
+      const int b = __builtin_amdgcn_readlane(lreg, j - lbase);
+      return (b >= blk_lo && b < blk_hi) ? b : -1;
     }
   };
 
@@ -215,78 +261,83 @@ void attn_fwd_kernel(AttnArgs a) {
   float m_run = -INFINITY;  // running max (log2 domain), shared by both lane halves
   float l_run = 0.f;        // this lane's partial row sum of the bf16 P it applied
 
-  // ---- tile copy through buffer loads: thread tid moves chunk
-  // (row0 + p * ROWS_PER_PASS, col8) of a tile.  Each tile gets its own
-  // descriptor (base at the tile, records = bytes left in the head), so rows
-  // past Lk read as zeros; the per-lane offsets stay in the range-checked
-  // vector offset.
-  const int row0 = tid / C::CPR, col8 = (tid % C::CPR) * 8;
+  // ---- direct-to-LDS tile loads: load i of wave w fills LDS bytes
+  // [(DPW w + i) KB, +1 KB); lane l writes 16 bytes at +16 l, i.e. physical
+  // chunk l % CPR of row RPD (DPW w + i) + l / CPR, and so reads the logical
+  // chunk that the XOR permutation puts there.  Each tile gets its own
+  // descriptor (records = bytes of the tile that exist), so rows past Lk and
+  // the tiles past the end of the list arrive as zeros.
+  uint32_t kdma[C::DPW], vdma[C::DPW];
+#pragma unroll
+  for (int i = 0; i < C::DPW; ++i) {
+    const int row = C::RPD * (C::DPW * wave + i) + lane / C::CPR, pos = lane % C::CPR;
+    kdma[i] = (uint32_t)(row * C::RB + 16 * (pos ^ k_swz<D, BLK>(row)));
+    vdma[i] = (uint32_t)(row * C::RB + 16 * (pos ^ v_swz<D, BLK>(row)));
+  }
   const uint16_t* const kbase = a.k + bh * a.lk * D;
   const uint16_t* const vbase = a.v + bh * a.lk * D;
-  constexpr uint32_t TILE_BYTES = BLK * D * 2;
-  uint32_t voff[C::CH];
-#pragma unroll
-  for (int p = 0; p < C::CH; ++p) voff[p] = (uint32_t)((row0 + p * C::ROWS_PER_PASS) * D + col8) * 2u;
-  const uint32_t last_bytes = (uint32_t)(a.lk - (int64_t)(a.n_k - 1) * BLK) * (D * 2);
-  auto tile_bytes = [&](int blk) -> uint32_t { return blk == a.n_k - 1 ? last_bytes : TILE_BYTES; };
-  uint4 kreg[C::CH], vreg[C::CH];
-  auto load_k = [&](int blk) {
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(kbase + (int64_t)blk * BLK * D, tile_bytes(blk));
-#pragma unroll
-    for (int p = 0; p < C::CH; ++p) kreg[p] = buf_load16(rs, voff[p], 0u);
+  const uint32_t last_bytes = (uint32_t)(a.lk - (int64_t)(a.n_k - 1) * BLK) * (uint32_t)C::RB;
+  auto tile_bytes = [&](int blk) -> uint32_t {
+    return blk < 0 ? 0u : (blk == a.n_k - 1 ? last_bytes : (uint32_t)C::TILE_BYTES);
   };
-  auto load_v = [&](int blk) {
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(vbase + (int64_t)blk * BLK * D, tile_bytes(blk));
+  auto dma = [&](const uint16_t* base, int blk, uint16_t* slot, const uint32_t* off) {
+    const i32x4 rs = raw_rsrc(base + (int64_t)(blk < 0 ? 0 : blk) * C::TILE, tile_bytes(blk));
+    const uint32_t m0 = lds_addr(slot) + (uint32_t)(C::DPW * wave) * 1024u;
 #pragma unroll
-    for (int p = 0; p < C::CH; ++p) vreg[p] = buf_load16(rs, voff[p], 0u);
-  };
-  uint16_t* const kst = smem + row0 * C::KLD + col8;
-  uint16_t* const vst = smem + 2 * C::K_ELEMS + row0 * C::VLD + col8;
-  auto store_k = [&](int buf) {
-#pragma unroll
-    for (int p = 0; p < C::CH; ++p)
-      *reinterpret_cast<uint4*>(kst + buf * C::K_ELEMS + p * C::ROWS_PER_PASS * C::KLD) = kreg[p];
-  };
-  auto store_v = [&](int buf) {
-#pragma unroll
-    for (int p = 0; p < C::CH; ++p)
-      *reinterpret_cast<uint4*>(vst + buf * C::V_ELEMS + p * C::ROWS_PER_PASS * C::VLD) = vreg[p];
+    for (int i = 0; i < C::DPW; ++i) dma16(m0 + 1024u * i, off[i], rs);
   };
 
-  // per-lane LDS read bases (buffer 0)
-  const uint16_t* const k_rd = smem + (kh * C::KH + l32) * C::KLD + 8 * hh;
-  const int grp = lane >> 4, sl = lane & 15;
-  const uint16_t* const v_rd =
-      smem + 2 * C::K_ELEMS + (kh * C::KH + 4 * hh + (sl >> 2)) * C::VLD + 16 * (grp & 1) + 4 * (sl & 3);
-
-  // ---- S^T = K Q^T for this wave's keys of the K tile in buffer kb
-  auto scores = [&](int kb, f32x16* acc) {
-    const uint16_t* ks = k_rd + kb * C::K_ELEMS;
+  // ---- per-lane LDS read offsets (bytes within a tile)
+  // K operand of S^T: row kh KH + 32 kt + l32, logical chunk 2 s + hh
+  uint32_t koff[C::DS];
+  {
+    const int r = kh * C::KH + l32;
 #pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt) {
+    for (int s = 0; s < C::DS; ++s) koff[s] = (uint32_t)(r * C::RB + 16 * ((2 * s + hh) ^ k_swz<D, BLK>(r)));
+  }
+  // V^T operand through the transpose read: in each 16-lane group g, source lane
+  // sl points at row R = kh KH + 4 hh + sl / 4 (+ 32 kt + 16 half + 8 for the
+  // second read), bytes 64 t + 32 (g % 2) + 8 (sl % 4), i.e. logical chunk
+  // 4 t + 2 (g % 2) + (sl % 4) / 2, half (sl % 2); lane j then receives
+  // V[R0 .. R0+3][4 c0 + j], four keys of one d column
+  uint32_t voff[C::DT];
+  {
+    const int grp = lane >> 4, sl = lane & 15;
+    const int r = kh * C::KH + 4 * hh + (sl >> 2);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[kt][e] = 0.f;
-#pragma unroll
-      for (int s = 0; s < C::DS; ++s) {
-        const uint4 u = *reinterpret_cast<const uint4*>(ks + kt * 32 * C::KLD + 16 * s);
-        acc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u), qf[s], acc[kt], 0, 0, 0);
-      }
+    for (int t = 0; t < C::DT; ++t) {
+      const int c = 4 * t + 2 * (grp & 1) + ((sl & 3) >> 1);
+      voff[t] = (uint32_t)(r * C::RB + 16 * (c ^ v_swz<D, BLK>(r)) + 8 * (sl & 1));
     }
+  }
+  auto kslot = [&](auto i) -> uint16_t* {
+    constexpr int I = decltype(i)::value;
+    if constexpr (I == 0) return ks0;
+    else if constexpr (I == 1) return ks1;
+    else return ks2;
+  };
+  auto vslot = [&](auto i) -> uint16_t* {
+    constexpr int I = decltype(i)::value;
+    if constexpr (I == 0) return vs0;
+    else return vs1;
+  };
+  auto lds_u4 = [](const uint16_t* slot, uint32_t byte_off) -> uint4 {
+    return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(slot) + byte_off);
   };
 
   const float sl2 = a.scale_log2;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // keys >= Lk of a partial last block get -inf scores
-  auto mask_tail = [&](f32x16* acc, int blk) {
+  // keys >= Lk of a partial last block, and every key of a -1 tile, get -inf
+  auto mask_tile = [&](f32x16* acc, int blk) {
     const int64_t key0 = (int64_t)blk * BLK;
-    if (key0 + BLK > a.lk) {
+    if (blk < 0 || key0 + BLK > a.lk) {
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = kh * C::KH + kt * 32 + 8 * (e / 4) + 4 * hh + (e % 4);
-          if (key0 + key >= a.lk) acc[kt][e] = -INFINITY;
+          if (blk < 0 || key0 + key >= a.lk) acc[kt][e] = -INFINITY;
         }
     }
   };
@@ -311,157 +362,184 @@ void attn_fwd_kernel(AttnArgs a) {
     }
   };
 
-  // ---- prologue: K of tiles 0 and 1 and V of tile 0 staged, K of tile 2 and
-  // V of tile 1 in flight, S of tile 0 computed and its max applied
-  int b0 = fetch_next();
-  int b1 = fetch_next();
-  int b2 = fetch_next();
-  f32x16 acc_s[C::KT];
-  if (b0 >= 0) {
-    load_k(b0);
-    load_v(b0);
-    store_k(0);
-    store_v(0);
-  }
-  if (b1 >= 0) {
-    load_k(b1);
-    store_k(1);
-    load_v(b1);
-  }
-  if (b2 >= 0) load_k(b2);
-  __syncthreads();
-  if (b0 >= 0) {
-    scores(0, acc_s);
-    mask_tail(acc_s, b0);
-    update_max(acc_s);
-  }
-  __syncthreads();  // K buffer 0 is rewritten in the first step
+  int b0 = -1, b1 = -1, b2 = -1, b3 = -1;  // blocks of tiles t .. t+3
+  f32x16 acc_s[C::KT];                     // S^T of tile t
 
-  // One step: P and O += P V of tile t (block b0) while the scores of tile t+1
-  // (block b1) run on the matrix cores.  The compute block has no branch, and
-  // sched_group_barrier interleaves each score MFMA with the exponentials of
-  // the current tile and each P V MFMA with a row-sum update, so the VALU work
-  // hides under the matrix-core work of the same wave.
-  auto step = [&](auto parity) {
-    constexpr int P = decltype(parity)::value;
-    f32x16 acc_n[C::KT];
-    const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
-
-    // K of tile t+1 (buffer 1-P; stale but harmless when there is no such tile)
-    uint4 kf[C::KT][C::DS];
-    const uint16_t* ks = k_rd + (1 - P) * C::K_ELEMS;
-#pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-      for (int s = 0; s < C::DS; ++s) kf[kt][s] = *reinterpret_cast<const uint4*>(ks + kt * 32 * C::KLD + 16 * s);
-
-    uint32_t pk[C::KT][8];  // bf16 pairs of P^T, per 32-key sub-tile
+  if (cnt > 0) {
+    // ---- prologue: K of tiles 0..2 and V of tile 0 in LDS, S of tile 0
+    // computed and its max applied
+    load_batch(0);
+    b0 = fetch(0);
+    b1 = fetch(1);
+    b2 = fetch(2);
+    b3 = fetch(3);
+    dma(kbase, b0, ks0, kdma);
+    dma(vbase, b0, vs0, vdma);
+    dma(kbase, b1, ks1, kdma);
+    dma(kbase, b2, ks2, kdma);
+    wait_vmcnt<0>();
+    __syncthreads();
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc_n[kt][e] = 0.f;
+      for (int e = 0; e < 16; ++e) acc_s[kt][e] = 0.f;
 #pragma unroll
       for (int s = 0; s < C::DS; ++s)
-        acc_n[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kt][s]), qf[s], acc_n[kt],
-                                                            0, 0, 0);
-#pragma unroll
-      for (int e = 0; e < 16; e += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
-        pk[kt][e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
-      }
+        acc_s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8, lds_u4(ks0, koff[s] + kt * 32 * C::RB)), qf[s], acc_s[kt], 0, 0, 0);
     }
+    mask_tile(acc_s, b0);
+    update_max(acc_s);
+    __syncthreads();  // K slot 0 receives tile 3 in the first step
 
-    // O^T += V^T P^T over 16-key k-steps (V tile of block b0 in buffer P)
-    const uint16_t* vs = v_rd + P * C::V_ELEMS;
+    // One step (T = t mod 6 fixes the slots): P and O += P V of tile t while
+    // the scores of tile t+1 run on the matrix cores.  The compute block has no
+    // branch, and sched_group_barrier interleaves each score MFMA with the
+    // exponentials of the current tile and each P V MFMA with a row-sum update,
+    // so the VALU work hides under the matrix-core work of the same wave.
+    int t = 0;
+    auto step = [&](auto tc) {
+      constexpr int T = decltype(tc)::value;
+      constexpr int KR = (T + 1) % 3, VR = T % 2;  // slots read: K(t+1), V(t)
+      constexpr int KW = T % 3, VW = (T + 1) % 2;  // slots filled: K(t+3), V(t+1)
+      uint16_t* const kr = kslot(std::integral_constant<int, KR>{});
+      uint16_t* const vr = vslot(std::integral_constant<int, VR>{});
+
+      // loads for the coming steps: V(t+1) (waited for at the end of this
+      // step) and K(t+3) (waited for one step later)
+      dma(vbase, b1, vslot(std::integral_constant<int, VW>{}), vdma);
+      dma(kbase, b3, kslot(std::integral_constant<int, KW>{}), kdma);
+
+      f32x16 acc_n[C::KT];
+      const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
+
+      uint4 kf[C::KT][C::DS];
 #pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt)
+      for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        // accumulators a = 8 half + i of sub-tile kt hold keys
-        //   base + 4 hh + i (i = 0..3) and base + 8 + 4 hh + (i - 4) (i = 4..7),
-        // base = kh * KH + 32 kt + 16 half; the two transpose reads fetch the
-        // same keys of V for d = 32 t + l % 32.
-        uint4 pu;
-        pu.x = pk[kt][4 * half + 0];
-        pu.y = pk[kt][4 * half + 1];
-        pu.z = pk[kt][4 * half + 2];
-        pu.w = pk[kt][4 * half + 3];
-        const bf16x8 pb = __builtin_bit_cast(bf16x8, pu);
+        for (int s = 0; s < C::DS; ++s) kf[kt][s] = lds_u4(kr, koff[s] + kt * 32 * C::RB);
+
+      uint32_t pk[C::KT][8];  // bf16 pairs of P^T, per 32-key sub-tile
 #pragma unroll
-        for (int t = 0; t < C::DT; ++t) {
-          const uint16_t* vr = vs + (32 * kt + 16 * half) * C::VLD + 32 * t;
-          const s16x4 v0 = lds_read_tr(vr);
-          const s16x4 v1 = lds_read_tr(vr + 8 * C::VLD);
-          const s16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-          acc_o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, acc_o[t], 0, 0, 0);
+      for (int kt = 0; kt < C::KT; ++kt) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc_n[kt][e] = 0.f;
+#pragma unroll
+        for (int s = 0; s < C::DS; ++s)
+          acc_n[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kt][s]), qf[s],
+                                                              acc_n[kt], 0, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
+          pk[kt][e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
+        }
+      }
+
+      // O^T += V^T P^T over 16-key k-steps
+#pragma unroll
+      for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          // accumulators a = 8 half + i of sub-tile kt hold keys
+          //   base + 4 hh + i (i = 0..3) and base + 8 + 4 hh + (i - 4) (i = 4..7),
+          // base = kh * KH + 32 kt + 16 half; the two transpose reads fetch the
+          // same keys of V for d = 32 t + l % 32.
+          uint4 pu;
+          pu.x = pk[kt][4 * half + 0];
+          pu.y = pk[kt][4 * half + 1];
+          pu.z = pk[kt][4 * half + 2];
+          pu.w = pk[kt][4 * half + 3];
+          const bf16x8 pb = __builtin_bit_cast(bf16x8, pu);
+#pragma unroll
+          for (int dt = 0; dt < C::DT; ++dt) {
+            const uint16_t* vp = reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(vr) + voff[dt] +
+                                                                   (32 * kt + 16 * half) * C::RB);
+            const s16x4 v0 = lds_read_tr(vp);
+            const s16x4 v1 = lds_read_tr(vp + 8 * D);
+            const s16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+            acc_o[dt] =
+                __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, acc_o[dt], 0, 0, 0);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][4 * half + i]), ones, l_run,
+                                                    false);
+        }
+      if constexpr (C::KT == 1 && C::DS == 8 && C::DT == 4) {
+        // K reads first; then 8 x (score MFMA + 5 VALU of the exponentials + 2 V
+        // transpose reads, so the V operands land while the exponentials run);
+        // then 8 x (P V MFMA + 1 row-sum VALU)
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][4 * half + i]), ones, l_run,
-                                                  false);
+        for (int i = 0; i < 8; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+        }
       }
-    if constexpr (C::KT == 1 && C::DS == 8 && C::DT == 4) {
-      // K reads first; then 8 x (score MFMA + 5 VALU of the exponentials + 2 V
-      // transpose reads, so the V operands land while the exponentials run);
-      // then 8 x (P V MFMA + 1 row-sum VALU)
-      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+
+      // scores of tile t+1: tail mask and running max (rescales O if needed)
+      if (t + 1 < cnt) {
+        mask_tile(acc_n, b1);
+        update_max(acc_n);
+      }
+
+      // V(t+1) has landed (only the K loads of this step may still be in
+      // flight); K(t+2) was issued one step earlier
+      wait_vmcnt<C::DPW>();
+      __syncthreads();
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      }
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
-      }
+      for (int kt = 0; kt < C::KT; ++kt) acc_s[kt] = acc_n[kt];
+      b0 = b1;
+      b1 = b2;
+      b2 = b3;
+      b3 = fetch(t + 4);
+    };
+
+    while (true) {
+      step(std::integral_constant<int, 0>{});
+      if (++t >= cnt) break;
+      step(std::integral_constant<int, 1>{});
+      if (++t >= cnt) break;
+      step(std::integral_constant<int, 2>{});
+      if (++t >= cnt) break;
+      step(std::integral_constant<int, 3>{});
+      if (++t >= cnt) break;
+      step(std::integral_constant<int, 4>{});
+      if (++t >= cnt) break;
+      step(std::integral_constant<int, 5>{});
+      if (++t >= cnt) break;
     }
-
-    // scores of tile t+1: tail mask and running max (rescales O if needed)
-    if (b1 >= 0) {
-      mask_tail(acc_n, b1);
-      update_max(acc_n);
-    }
-
-    // stage K of t+2 and V of t+1, start the loads of K of t+3 and V of t+2
-    if (b2 >= 0) store_k(P);
-    if (b1 >= 0) store_v(1 - P);
-    const int b3 = fetch_next();
-    if (b3 >= 0) load_k(b3);
-    if (b2 >= 0) load_v(b2);
-    __syncthreads();
-#pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt) acc_s[kt] = acc_n[kt];
-    b0 = b1;
-    b1 = b2;
-    b2 = b3;
-  };
-
-  while (b0 >= 0) {
-    step(std::integral_constant<int, 0>{});
-    if (b0 < 0) break;
-    step(std::integral_constant<int, 1>{});
+    wait_vmcnt<0>();  // loads past the end of the list still write LDS
   }
+  __syncthreads();
 
-  // ---- merge the two key halves of each query slice, then write O and lse
+  // ---- merge the two key halves of each query slice, then write O and lse.
+  // Key half 1 of slice qs leaves its 16 DT accumulators per lane in
+  // K slot qs*16 DT*256 bytes / TILE_BYTES (slots 0 and 1) and (m, l) in V slot 0.
   l_run = half_swap_sum(l_run);  // both lane halves now hold the slice's partial sum
-  float* mrg = reinterpret_cast<float*>(smem);  // [NQS][2 + 16 DT][64] floats; tile buffers are free now
-  constexpr int MR = 2 + 16 * C::DT;
-  static_assert(C::NQS * MR * 64 * 4 <= (2 * C::K_ELEMS + 2 * C::V_ELEMS) * 2, "merge buffer fits in LDS");
-  float* my = mrg + qs * MR * 64;
+  constexpr int OB = 16 * C::DT * 64 * 4;  // bytes of one slice's accumulators
+  static_assert(C::NQS * OB <= 2 * C::TILE_BYTES, "merge buffer fits in K slots 0 and 1");
+  float* my_o = reinterpret_cast<float*>(reinterpret_cast<char*>((qs * OB) / C::TILE_BYTES == 0 ? ks0 : ks1) +
+                                         (qs * OB) % C::TILE_BYTES);
+  float* my_ml = reinterpret_cast<float*>(vs0) + qs * 2 * 64;
   if (kh == 1) {
-    my[0 * 64 + lane] = m_run;
-    my[1 * 64 + lane] = l_run;
+    my_ml[0 * 64 + lane] = m_run;
+    my_ml[1 * 64 + lane] = l_run;
 #pragma unroll
     for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) my[(2 + 16 * t + e) * 64 + lane] = acc_o[t][e];
+      for (int e = 0; e < 16; ++e) my_o[(16 * t + e) * 64 + lane] = acc_o[t][e];
   }
   __syncthreads();
   if (kh == 0) {
-    const float m1 = my[0 * 64 + lane], l1 = my[1 * 64 + lane];
+    const float m1 = my_ml[0 * 64 + lane], l1 = my_ml[1 * 64 + lane];
     const float mm = fmaxf(m_run, m1);
     const float a0 = m_run == -INFINITY ? 0.f : exp2f(m_run - mm);
     const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - mm);
@@ -478,7 +556,7 @@ void attn_fwd_kernel(AttnArgs a) {
           f16x4 w;
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            w[e] = (_Float16)((acc_o[t][4 * g + e] * a0 + my[(2 + 16 * t + 4 * g + e) * 64 + lane] * a1) * inv);
+            w[e] = (_Float16)((acc_o[t][4 * g + e] * a0 + my_o[(16 * t + 4 * g + e) * 64 + lane] * a1) * inv);
           *reinterpret_cast<f16x4*>(po + d) = w;
         }
       if (hh == 0) {
@@ -496,7 +574,7 @@ void attn_fwd_kernel(AttnArgs a) {
           float o[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            o[e] = (acc_o[t][4 * g + e] * a0 + my[(2 + 16 * t + 4 * g + e) * 64 + lane] * a1) * inv;
+            o[e] = (acc_o[t][4 * g + e] * a0 + my_o[(16 * t + 4 * g + e) * 64 + lane] * a1) * inv;
           uint2 w;
           w.x = pack2_bf16(o[0], o[1]);
           w.y = pack2_bf16(o[2], o[3]);
