@@ -187,6 +187,17 @@ void attn_fwd_kernel(AttnArgs a) {
   const int qs = wave % C::NQS;   // query slice
   const int kh = wave / C::NQS;   // key half
 
+  // ---- Q fragment (B operand of S^T = K Q^T): Q[q][16 s + 8 hh .. +7]
+  const int64_t q_row = (int64_t)qb * BLK + qs * 32 + l32;
+  const bool q_ok = q_row < a.lq;
+  const uint16_t* qp = a.q + (bh * a.lq + (q_ok ? q_row : 0)) * D;
+  bf16x8 qf[C::DS];
+#pragma unroll
+  for (int s = 0; s < C::DS; ++s) {
+    const uint4 u = q_ok ? *reinterpret_cast<const uint4*>(qp + 16 * s + 8 * hh) : make_uint4(0, 0, 0, 0);
+    qf[s] = __builtin_bit_cast(bf16x8, u);
+  }
+
   // ---- the list positions [pos_lo, pos_lo + cnt) that hold the blocks of
   // [blk_lo, blk_hi): an ascending list has them after the entries < blk_lo and
   // before the entries >= blk_hi (every wave counts them itself)
@@ -200,16 +211,24 @@ void attn_fwd_kernel(AttnArgs a) {
     int nblk = a.kv_num_blocks[r];
     nblk = nblk < 0 ? 0 : (nblk > a.stride ? a.stride : nblk);
     list = a.kv_indices + r * a.stride;
+    // 64 x U entries per pass, all loads independent (one memory latency per
+    // pass); the counts come from ballots, so they are wave-uniform at once
+    constexpr int U = 12;
     int c_lo = 0, c_hi = 0;
-    for (int i = lane; i < nblk; i += 64) {
-      const int j = list[i];
-      c_lo += j < blk_lo;
-      c_hi += j < blk_hi;
-    }
+    // (the first pass does not wait for the count: it reads up to the stride)
+    for (int base = 0; base == 0 || base < nblk; base += 64 * U) {
+      int v[U];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      c_lo += __shfl_xor(c_lo, off, 64);
-      c_hi += __shfl_xor(c_hi, off, 64);
+      for (int u = 0; u < U; ++u) {
+        const int i = base + 64 * u + lane;
+        v[u] = i < a.stride ? list[i] : 0x7fffffff;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bool in = base + 64 * u + lane < nblk;
+        c_lo += __builtin_popcountll(__builtin_amdgcn_ballot_w64(in && v[u] < blk_lo));
+        c_hi += __builtin_popcountll(__builtin_amdgcn_ballot_w64(in && v[u] < blk_hi));
+      }
     }
     pos_lo = __builtin_amdgcn_readfirstlane(c_lo);
     cnt = __builtin_amdgcn_readfirstlane(c_hi) - pos_lo;
@@ -241,17 +260,6 @@ void attn_fwd_kernel(AttnArgs a) {
       return (b >= blk_lo && b < blk_hi) ? b : -1;
     }
   };
-
-  // ---- Q fragment (B operand of S^T = K Q^T): Q[q][16 s + 8 hh .. +7]
-  const int64_t q_row = (int64_t)qb * BLK + qs * 32 + l32;
-  const bool q_ok = q_row < a.lq;
-  const uint16_t* qp = a.q + (bh * a.lq + (q_ok ? q_row : 0)) * D;
-  bf16x8 qf[C::DS];
-#pragma unroll
-  for (int s = 0; s < C::DS; ++s) {
-    const uint4 u = q_ok ? *reinterpret_cast<const uint4*>(qp + 16 * s + 8 * hh) : make_uint4(0, 0, 0, 0);
-    qf[s] = __builtin_bit_cast(bf16x8, u);
-  }
 
   f32x16 acc_o[C::DT];
 #pragma unroll
@@ -341,15 +349,34 @@ void attn_fwd_kernel(AttnArgs a) {
         }
     }
   };
-  // running max for a new score tile, with lazy rescaling: O and l are only
-  // rescaled when a query's maximum grows by more than 2^8
-  auto update_max = [&](const f32x16* acc) {
+  int b1 = -1, b2 = -1, b3 = -1, b4 = -1;  // blocks of tiles t+1 .. t+4
+  f32x16 acc_s[C::KT];                     // S^T of tile t
+
+  // S^T of one K tile (LDS slot ks) into acc
+  auto scores = [&](const uint16_t* ks, f32x16* acc) {
+#pragma unroll
+    for (int kt = 0; kt < C::KT; ++kt) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[kt][e] = 0.f;
+#pragma unroll
+      for (int s = 0; s < C::DS; ++s)
+        acc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8, lds_u4(ks, koff[s] + kt * 32 * C::RB)), qf[s], acc[kt], 0, 0, 0);
+    }
+  };
+  // the tile's max logit (log2 domain) of the lane's query over both lane halves
+  auto tile_max = [&](const f32x16* acc) -> float {
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[kt][e]);
-    mx = half_swap_max(mx) * sl2;  // the tile's max logit (log2 domain) for the lane's query
+    return mx;
+  };
+  // lazy rescaling: O and l are only rescaled when a query's running maximum
+  // grows by more than 2^8
+  auto apply_max = [&](float mx) {
+    mx = half_swap_max(mx) * sl2;
     if (__any(mx > m_run + 8.0f)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
@@ -361,64 +388,57 @@ void attn_fwd_kernel(AttnArgs a) {
       m_run = m_new;
     }
   };
-
-  int b0 = -1, b1 = -1, b2 = -1, b3 = -1;  // blocks of tiles t .. t+3
-  f32x16 acc_s[C::KT];                     // S^T of tile t
+  auto needs_mask = [&](int blk) { return blk < 0 || (int64_t)blk * BLK + BLK > a.lk; };
 
   if (cnt > 0) {
-    // ---- prologue: K of tiles 0..2 and V of tile 0 in LDS, S of tile 0
-    // computed and its max applied
+    // ---- prologue.  The loads follow the order of the steady state (K(j+4)
+    // after the first barrier of step j, V(j+2) after the second), so that the
+    // vmcnt thresholds of the step hold from the first step on.
     load_batch(0);
-    b0 = fetch(0);
+    const int b0 = fetch(0);
     b1 = fetch(1);
     b2 = fetch(2);
     b3 = fetch(3);
+    b4 = fetch(4);
     dma(kbase, b0, ks0, kdma);
-    dma(vbase, b0, vs0, vdma);
     dma(kbase, b1, ks1, kdma);
     dma(kbase, b2, ks2, kdma);
-    wait_vmcnt<0>();
+    dma(vbase, b0, vs0, vdma);
+    wait_vmcnt<3 * C::DPW>();  // K(0)
     __syncthreads();
-#pragma unroll
-    for (int kt = 0; kt < C::KT; ++kt) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc_s[kt][e] = 0.f;
-#pragma unroll
-      for (int s = 0; s < C::DS; ++s)
-        acc_s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8, lds_u4(ks0, koff[s] + kt * 32 * C::RB)), qf[s], acc_s[kt], 0, 0, 0);
-    }
-    mask_tile(acc_s, b0);
-    update_max(acc_s);
-    __syncthreads();  // K slot 0 receives tile 3 in the first step
+    scores(ks0, acc_s);
+    if (needs_mask(b0)) mask_tile(acc_s, b0);
+    apply_max(tile_max(acc_s));
+    __syncthreads();  // K slot 0 is free
+    dma(kbase, b3, ks0, kdma);
+    wait_vmcnt<3 * C::DPW>();  // K(1)
+    __syncthreads();
+    dma(vbase, b1, vs1, vdma);
 
-    // One step (T = t mod 6 fixes the slots): P and O += P V of tile t while
-    // the scores of tile t+1 run on the matrix cores.  The compute block has no
-    // branch, and sched_group_barrier interleaves each score MFMA with the
-    // exponentials of the current tile and each P V MFMA with a row-sum update,
-    // so the VALU work hides under the matrix-core work of the same wave.
+    // One step (T = t mod 6 fixes the slots), in two phases:
+    //   A: the scores of tile t+1 on the matrix cores while the exponentials of
+    //      tile t run; then V(t) is waited for, a barrier releases K slot
+    //      (t+1) % 3, and K(t+4) is loaded into it (it has 2.5 steps to land);
+    //   B: O += P V of tile t and the running max of tile t+1; then K(t+2) is
+    //      waited for, a barrier releases V slot t % 2, and V(t+2) is loaded
+    //      into it (1.5 steps to land).
+    // Each phase is branch-free, and sched_group_barrier interleaves its MFMAs
+    // with its VALU work so that the latter hides under the matrix cores.
     int t = 0;
     auto step = [&](auto tc) {
       constexpr int T = decltype(tc)::value;
-      constexpr int KR = (T + 1) % 3, VR = T % 2;  // slots read: K(t+1), V(t)
-      constexpr int KW = T % 3, VW = (T + 1) % 2;  // slots filled: K(t+3), V(t+1)
-      uint16_t* const kr = kslot(std::integral_constant<int, KR>{});
-      uint16_t* const vr = vslot(std::integral_constant<int, VR>{});
+      constexpr int KS = (T + 1) % 3, VS = T % 2;
+      uint16_t* const kr = kslot(std::integral_constant<int, KS>{});
+      uint16_t* const vr = vslot(std::integral_constant<int, VS>{});
 
-      // loads for the coming steps: V(t+1) (waited for at the end of this
-      // step) and K(t+3) (waited for one step later)
-      dma(vbase, b1, vslot(std::integral_constant<int, VW>{}), vdma);
-      dma(kbase, b3, kslot(std::integral_constant<int, KW>{}), kdma);
-
+      // ---- phase A
       f32x16 acc_n[C::KT];
       const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
-
       uint4 kf[C::KT][C::DS];
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
         for (int s = 0; s < C::DS; ++s) kf[kt][s] = lds_u4(kr, koff[s] + kt * 32 * C::RB);
-
       uint32_t pk[C::KT][8];  // bf16 pairs of P^T, per 32-key sub-tile
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt) {
@@ -435,8 +455,21 @@ void attn_fwd_kernel(AttnArgs a) {
           pk[kt][e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
         }
       }
+      if constexpr (C::KT == 1 && C::DS == 8) {
+        // the K reads, then 8 x (score MFMA + 5 VALU of the exponentials)
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);  // the phase ends here
+      wait_vmcnt<2 * C::DPW>();  // V(t)
+      __syncthreads();
+      dma(kbase, b4, kr, kdma);
 
-      // O^T += V^T P^T over 16-key k-steps
+      // ---- phase B: O^T += V^T P^T over 16-key k-steps
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
@@ -466,40 +499,42 @@ void attn_fwd_kernel(AttnArgs a) {
             l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][4 * half + i]), ones, l_run,
                                                     false);
         }
-      if constexpr (C::KT == 1 && C::DS == 8 && C::DT == 4) {
-        // K reads first; then 8 x (score MFMA + 5 VALU of the exponentials + 2 V
-        // transpose reads, so the V operands land while the exponentials run);
-        // then 8 x (P V MFMA + 1 row-sum VALU)
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+      float mx = tile_max(acc_n);
+      if constexpr (C::KT == 1 && C::DT == 4) {
+        // the first two MFMAs' V reads, then 6 x (P V MFMA + the V reads of the
+        // MFMA two ahead + 2 VALU), then 2 x (MFMA + 2 VALU); the VALU work is
+        // the row sums and the max of the next tile
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < 6; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
         }
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < 2; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
         }
       }
-
-      // scores of tile t+1: tail mask and running max (rescales O if needed)
       if (t + 1 < cnt) {
-        mask_tile(acc_n, b1);
-        update_max(acc_n);
+        if (needs_mask(b1)) {
+          mask_tile(acc_n, b1);
+          mx = tile_max(acc_n);
+        }
+        apply_max(mx);
       }
-
-      // V(t+1) has landed (only the K loads of this step may still be in
-      // flight); K(t+2) was issued one step earlier
-      wait_vmcnt<C::DPW>();
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vmcnt<3 * C::DPW>();  // K(t+2)
       __syncthreads();
+      dma(vbase, b2, vr, vdma);
+
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt) acc_s[kt] = acc_n[kt];
-      b0 = b1;
       b1 = b2;
       b2 = b3;
-      b3 = fetch(t + 4);
+      b3 = b4;
+      b4 = fetch(t + 5);
     };
 
     while (true) {
