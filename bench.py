@@ -44,11 +44,18 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def executed_flops(num_blocks: np.ndarray, lq: int, lk: int, block: int, d: int) -> float:
-    """Sum over (b, h, i) of 4 * rows_i * keys(A_i) * D with full blocks (the
-    shapes measured here are multiples of the block size)."""
-    assert lq % block == 0 and lk % block == 0
-    return float(num_blocks.astype(np.float64).sum()) * 4.0 * block * block * d
+def executed_flops(num_blocks: np.ndarray, last_entries: np.ndarray, lq: int, lk: int, block: int,
+                   d: int) -> float:
+    """Sum over (b, h, i) of 4 * rows_i * keys(A_i) * D, where rows_i is the
+    number of real query rows of block i and keys(A_i) counts only real keys
+    (the last key block may be partial; lists are ascending, so it is present
+    exactly when it is the row's last entry)."""
+    n_q, n_k = -(-lq // block), -(-lk // block)
+    rows = np.full(n_q, float(block))
+    rows[-1] = lq - (n_q - 1) * block
+    short = block - (lk - (n_k - 1) * block)  # missing keys of the last key block
+    keys = num_blocks.astype(np.float64) * block - short * ((last_entries == n_k - 1) & (num_blocks > 0))
+    return float((keys * rows).sum()) * 4.0 * d
 
 
 def traffic_from_profile() -> dict | None:
@@ -160,7 +167,10 @@ class Runner:
 
     def flops(self) -> float:
         B, H, Lq, Lk, D = self.shape
-        return executed_flops(self.num.cpu().numpy(), Lq, Lk, self.w.block, D)
+        num = self.num.cpu().numpy()
+        idx = self.idx.cpu().numpy()
+        last = np.take_along_axis(idx, np.clip(num - 1, 0, None)[..., None].astype(np.int64), axis=-1)[..., 0]
+        return executed_flops(num, last, Lq, Lk, self.w.block, D)
 
     def dense_flops(self) -> float:
         B, H, Lq, Lk, D = self.shape
@@ -177,6 +187,7 @@ def main() -> int:
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-pyramid", action="store_true")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache selector timing")
     ap.add_argument("--gen-workers", type=int, default=None,
                     help="input-generation processes (1 = in-process; use 1 under a profiler)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -271,8 +282,13 @@ def main() -> int:
         },
         "breakdown_ms": {
             "score_blocks": float(np.mean(sel_ms)),
+            "score_blocks_median": float(np.median(sel_ms)),
+            "score_blocks_min": float(np.min(sel_ms)),
+            "score_blocks_p90": float(np.percentile(sel_ms, 90)),
             "sparse_attn_fwd": att_avg,
+            "sparse_attn_fwd_median": float(np.median(att_ms)),
             "sparse_attn_fwd_min": float(np.min(att_ms)),
+            "sparse_attn_fwd_p90": float(np.percentile(att_ms, 90)),
         },
         "roofline": {
             "bound": "mfma",
@@ -286,6 +302,26 @@ def main() -> int:
     }
     if tr is not None:
         out["roofline"]["traffic_detail_bytes"] = tr
+
+    if not args.no_cold:
+        # the selector from cold caches: a 512 MiB write evicts L2 and MALL
+        # before each rep, so Q and K come from HBM
+        scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
+        cold = []
+        for _ in range(5):
+            scratch.fill_(1)
+            a, b = r.ev(), r.ev()
+            a.record()
+            r.score()
+            b.record()
+            torch.cuda.synchronize()
+            cold.append(a.elapsed_time(b))
+        del scratch
+        read_bytes = 2.0 * B * H * (Lq + Lk) * D  # Q and K, bf16, read once by the pooling kernel
+        out["breakdown_ms"]["score_blocks_cold_median"] = float(np.median(cold))
+        out["breakdown_ms"]["score_blocks_cold_min"] = float(np.min(cold))
+        log(f"selector from cold caches: median {np.median(cold):.3f} ms "
+            f"({read_bytes / (np.median(cold) * 1e-3) / 1e12:.2f} TB/s of Q+K over the whole selector call)")
 
     dense_ms = None
     if not args.no_dense:

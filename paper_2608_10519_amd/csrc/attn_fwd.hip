@@ -455,13 +455,18 @@ void attn_fwd_kernel(AttnArgs a) {
           pk[kt][e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
         }
       }
-      if constexpr (C::KT == 1 && C::DS == 8) {
-        // the K reads, then 8 x (score MFMA + 5 VALU of the exponentials)
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+      if constexpr (C::DS == 8) {
+        // per 32-key sub-tile: its K reads, then 8 x (score MFMA + 5 VALU of
+        // the exponentials); sub-tiles one after the other keeps one sub-tile's
+        // K operands live at a time
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+        for (int kt = 0; kt < C::KT; ++kt) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+          }
         }
       }
       __builtin_amdgcn_sched_barrier(0);  // the phase ends here
@@ -500,13 +505,13 @@ void attn_fwd_kernel(AttnArgs a) {
                                                     false);
         }
       float mx = tile_max(acc_n);
-      if constexpr (C::KT == 1 && C::DT == 4) {
-        // the first two MFMAs' V reads, then 6 x (P V MFMA + the V reads of the
-        // MFMA two ahead + 2 VALU), then 2 x (MFMA + 2 VALU); the VALU work is
-        // the row sums and the max of the next tile
+      if constexpr (C::DT == 4) {
+        // the first two MFMAs' V reads, then (P V MFMA + the V reads of the
+        // MFMA two ahead + 2 VALU) for all but the last two MFMAs, then 2 x (MFMA
+        // + 2 VALU); the VALU work is the row sums and the max of the next tile
         __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-        for (int i = 0; i < 6; ++i) {
+        for (int i = 0; i < 8 * C::KT - 2; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
           __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);

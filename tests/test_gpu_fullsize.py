@@ -89,3 +89,17 @@ def test_720p_per_head_budget_sweep_parity(gpu_lib):
         assert (num[0, h] == 8 + O.budget_k(float(budgets[h]), n_sel)).all()
     _check_heads(w, data, keep, num, idx, o, lse, heads=[int(np.argmax(budgets))], qblocks=[3, 1000],
                  budgets=budgets)
+
+
+def test_720p_block_128_parity(gpu_lib):
+    """The paper's deployed block size at the 720p shape: 72000 = 562.5 x 128,
+    so the text segment [72000, 72512) straddles blocks 562 and 566 and all of
+    blocks 562..566 are forced (Section 5.1's intersection rule at scale)."""
+    w = P720.with_(name="720p-b128", block=128)
+    data, keep, num, idx, o, lse = _run_full(gpu_lib, w, w.density)
+    n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
+    keep_set = O.keep_blocks(keep, w.lk, w.block)
+    assert sorted(keep_set) == [562, 563, 564, 565, 566]
+    assert (num == 5 + O.budget_k(w.density, n_k - 5)).all()
+    _check_heads(w, data, keep, num, idx, o, lse, heads=[0, 11], qblocks=[0, 281, n_q - 1],
+                 budgets=np.full(w.heads, w.density))
