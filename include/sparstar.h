@@ -167,6 +167,41 @@ int sparstar_dense_attn_fwd(const void* q, const void* k, const void* v, int B, 
                             int block_size, float softmax_scale, void* o, float* lse, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/*
+ * Forced token ranges of Eq. 3 for clip `clip` (1-based; Section 5.2,
+ * "Clip-Dependent Retained and Selectable Blocks"): clip 1 keeps the text and
+ * the final image-pyramid reference dense, a clip c >= 2 keeps only the text
+ * (its preceding-clip reference blocks are ranked jointly with the current
+ * ones).  Host only; the result feeds the `keep` argument of
+ * sparstar_score_blocks and sparstar_kv_stride.
+ *   text, ref   token ranges [begin, end) of the two segments in the key
+ *               sequence (0 <= begin <= end)
+ *   out, cap    receive the ranges, text first; cap >= 2 always suffices
+ * Returns the number of ranges written (1 or 2), or SPARSTAR_ERR_INVALID_ARG
+ * for clip < 1, a malformed range, a NULL `out` or a `cap` below the count.
+ */
+int sparstar_clip_keep_ranges(int clip, sparstar_range text, sparstar_range ref, sparstar_range* out, int cap);
+
+/*
+ * Scale-wise density schedule (Section 5.2, Eq. 5, and the supplement's
+ * "Sparsity Schedule and Later-Clip Policy"): the n_finest finest scales of a
+ * clip group, in order of increasing token count, get the densities
+ * finest_rho, and the lookup is by query length, so any scale with the token
+ * count of a sparsified scale shares its density; all other scales stay dense.
+ * The paper's 720p setting sparsifies the four finest scales with
+ * (0.625, 0.1875, 0.1875, 0.09375) (native scales s26-s29 of clip 1; s38-s41 of
+ * clip 2 in the ten-second evaluation, whose clip 1 is dense).  Host only.
+ *   scale_lq     [n_scales] query length of every scale of the clip group, in
+ *                generation order
+ *   finest_rho   [n_finest] densities in [0, 1] of the last n_finest scales
+ *   rho_out      [n_scales] receives rho of each scale, or -1.0 for a dense scale
+ * Returns SPARSTAR_OK, or SPARSTAR_ERR_INVALID_ARG for n_finest > n_scales,
+ * negative counts, NULL arrays with positive counts, a density outside [0, 1]
+ * or two sparsified scales with equal token counts and different densities.
+ */
+int sparstar_scale_densities(const int64_t* scale_lq, int n_scales, const double* finest_rho, int n_finest,
+                             double* rho_out);
+
 /* Message for the last non-OK return on this thread ("" if none). */
 const char* sparstar_last_error(void);
 

@@ -14,6 +14,7 @@ from .sparstar_oracle import (  # noqa: F401
     partition,
     pool,
     retained_support,
+    scale_densities,
     segment_blocks,
     select,
     selectable_blocks,

@@ -103,6 +103,31 @@ def selectable_blocks(keep_set: list[int], lk: int, b: int) -> list[int]:
 
 
 # --------------------------------------------------------------------------
+# Section 5.2 and the supplement's sparsity schedule: scale-wise densities
+# --------------------------------------------------------------------------
+def scale_densities(scale_lq: list[int], finest_rho: list[float]) -> list[float | None]:
+    """rho_{c,s} for every scale s of one clip group, in generation order.
+
+    The schedule assigns the given densities to the len(finest_rho) finest
+    scales (the last ones, in order of increasing token count) and is a lookup
+    by query length: every scale whose token count equals that of a sparsified
+    scale gets that scale's density (scales with equal token counts share a
+    density); all other scales stay dense (None).  Two sparsified scales with
+    equal token counts but different densities contradict the lookup."""
+    n = len(finest_rho)
+    if n > len(scale_lq):
+        raise ValueError("more densities than scales")
+    table: dict[int, float] = {}
+    for lq, rho in zip(scale_lq[len(scale_lq) - n:], finest_rho):
+        if not (0.0 <= rho <= 1.0):
+            raise ValueError("densities lie in [0, 1]")
+        if table.get(lq, rho) != rho:
+            raise ValueError("equal token counts with different densities")
+        table[lq] = rho
+    return [table.get(lq) for lq in scale_lq]
+
+
+# --------------------------------------------------------------------------
 # Eq. (5): the budget
 # --------------------------------------------------------------------------
 def budget_k(rho: float, n_sel: int) -> int:

@@ -136,6 +136,49 @@ extern "C" int64_t sparstar_kv_stride(int H, int64_t Lk, int block_size, const d
   return plan.n_keep_blocks + plan.max_k;
 }
 
+extern "C" int sparstar_clip_keep_ranges(int clip, sparstar_range text, sparstar_range ref, sparstar_range* out,
+                                         int cap) {
+  if (clip < 1) return fail(SPARSTAR_ERR_INVALID_ARG, "clip index starts at 1 (got %d)", clip);
+  if (text.begin < 0 || text.begin > text.end || ref.begin < 0 || ref.begin > ref.end)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "ranges need 0 <= begin <= end");
+  const int n = clip == 1 ? 2 : 1;  // Eq. 3: text and reference for clip 1, text only after
+  if (!out || cap < n) return fail(SPARSTAR_ERR_INVALID_ARG, "out needs room for %d ranges", n);
+  out[0] = text;
+  if (n == 2) out[1] = ref;
+  ok();
+  return n;
+}
+
+extern "C" int sparstar_scale_densities(const int64_t* scale_lq, int n_scales, const double* finest_rho, int n_finest,
+                                        double* rho_out) {
+  if (n_scales < 0 || n_finest < 0 || n_finest > n_scales)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "need 0 <= n_finest <= n_scales (got %d, %d)", n_finest, n_scales);
+  if (n_scales > 0 && (!scale_lq || !rho_out)) return fail(SPARSTAR_ERR_INVALID_ARG, "null scale arrays");
+  if (n_finest > 0 && !finest_rho) return fail(SPARSTAR_ERR_INVALID_ARG, "null densities");
+  // lookup table query length -> density, from the finest scales
+  std::vector<std::pair<int64_t, double>> table;
+  for (int i = 0; i < n_finest; ++i) {
+    const double rho = finest_rho[i];
+    if (!(rho >= 0.0 && rho <= 1.0)) return fail(SPARSTAR_ERR_INVALID_ARG, "density %g outside [0, 1]", rho);
+    const int64_t lq = scale_lq[n_scales - n_finest + i];
+    bool found = false;
+    for (const auto& e : table)
+      if (e.first == lq) {
+        if (e.second != rho)
+          return fail(SPARSTAR_ERR_INVALID_ARG, "scales of %lld tokens given densities %g and %g", (long long)lq,
+                      e.second, rho);
+        found = true;
+      }
+    if (!found) table.push_back({lq, rho});
+  }
+  for (int s = 0; s < n_scales; ++s) {
+    rho_out[s] = -1.0;
+    for (const auto& e : table)
+      if (e.first == scale_lq[s]) rho_out[s] = e.second;
+  }
+  return ok();
+}
+
 extern "C" const char* sparstar_last_error(void) { return g_error.c_str(); }
 
 struct WsLayout {

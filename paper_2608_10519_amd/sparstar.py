@@ -61,6 +61,10 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.sparstar_dense_attn_fwd.restype = c_i
     lib.sparstar_last_error.argtypes = []
     lib.sparstar_last_error.restype = ctypes.c_char_p
+    lib.sparstar_clip_keep_ranges.argtypes = [c_i, Range, Range, c_rp, c_i]
+    lib.sparstar_clip_keep_ranges.restype = c_i
+    lib.sparstar_scale_densities.argtypes = [ctypes.POINTER(ctypes.c_int64), c_i, c_dp, c_i, c_dp]
+    lib.sparstar_scale_densities.restype = c_i
     if path is None:
         _lib = lib
     return lib
@@ -124,6 +128,30 @@ def sparstar_kv_stride(H: int, Lk: int, block_size: int, budget, keep=()) -> int
     if r < 0:
         raise SparstarError("sparstar_kv_stride", r, last_error())
     return r
+
+
+# The paper's 720p schedule: densities of the four finest scales, in order of
+# increasing token count (Section 5.2; supplement, sparsity schedule).
+PAPER_720P_FINEST_DENSITIES = (0.625, 0.1875, 0.1875, 0.09375)
+
+
+def sparstar_clip_keep_ranges(clip: int, text: tuple[int, int], ref: tuple[int, int]) -> list[tuple[int, int]]:
+    """Forced token ranges of Eq. 3 for clip `clip` (text first)."""
+    out = (Range * 2)()
+    n = load().sparstar_clip_keep_ranges(int(clip), Range(*map(int, text)), Range(*map(int, ref)), out, 2)
+    if n < 0:
+        raise SparstarError("sparstar_clip_keep_ranges", n, last_error())
+    return [(out[i].begin, out[i].end) for i in range(n)]
+
+
+def sparstar_scale_densities(scale_lq: Sequence[int], finest_rho: Sequence[float]) -> list[float | None]:
+    """rho of every scale of one clip group (None: the scale stays dense)."""
+    n, m = len(scale_lq), len(finest_rho)
+    lq = (ctypes.c_int64 * max(n, 1))(*map(int, scale_lq))
+    rho = (ctypes.c_double * max(m, 1))(*map(float, finest_rho))
+    out = (ctypes.c_double * max(n, 1))()
+    _check("sparstar_scale_densities", load().sparstar_scale_densities(lq, n, rho, m, out))
+    return [None if out[i] < 0 else out[i] for i in range(n)]
 
 
 def sparstar_score_blocks(q: torch.Tensor, k: torch.Tensor, block_size: int, budget, keep=(), *,
