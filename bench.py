@@ -188,6 +188,7 @@ def main() -> int:
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-pyramid", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache selector timing")
+    ap.add_argument("--no-b128", action="store_true", help="skip the 720p run at block size 128")
     ap.add_argument("--gen-workers", type=int, default=None,
                     help="input-generation processes (1 = in-process; use 1 under a profiler)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -217,6 +218,8 @@ def main() -> int:
     log(f"generating {w.name}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk} rho={w.density}")
     t0 = time.perf_counter()
     data = generate(w, workers=args.gen_workers)
+    w128 = w.with_(name="720p-b128", block=128)
+    b128_data = None if args.no_b128 else generate(w128, workers=args.gen_workers)
     sweep_data = None if args.no_sweep else generate(SWEEP, workers=args.gen_workers)
     pyr = [] if args.no_pyramid else [(pw, sparse, generate(pw, workers=args.gen_workers))
                                       for pw, sparse in pyramid_scales()]
@@ -334,6 +337,20 @@ def main() -> int:
             "speedup_sparse_fwd_only": dense_ms / att_avg,
         }
         log(f"dense {dense_ms:.2f} ms -> speedup {dense_ms / ms_step:.2f}x (step), {dense_ms / att_avg:.2f}x (fwd)")
+
+    if b128_data is not None:
+        log("720p at the paper's deployed block size 128")
+        rb = Runner(S, torch, w128, *b128_data, w128.density)
+        sc = float(np.median(rb.timed(rb.score, 5)))
+        sp = float(np.median(rb.timed(rb.sparse, 5)))
+        dn = float(np.median(rb.timed(rb.dense, 2)))
+        fl = rb.flops()
+        out["block_128"] = {"score_ms": sc, "sparse_fwd_ms": sp, "executed_tflop": fl / 1e12,
+                            "tflops": fl / (sp * 1e-3) / 1e12, "kv_blocks_per_row": int(rb.num.max().item()),
+                            "dense_ms": dn, "dense_tflops": rb.dense_flops() / (dn * 1e-3) / 1e12,
+                            "speedup_vs_dense_step": dn / (sc + sp)}
+        log(f"  b=128: score {sc:.3f} ms, sparse {sp:.2f} ms ({fl / (sp * 1e-3) / 1e12:.0f} TFLOP/s), dense {dn:.1f} ms")
+        del rb
 
     if sweep_data is not None:
         log("density sweep (per-head budgets U[0.5, 1.5] x rho)")

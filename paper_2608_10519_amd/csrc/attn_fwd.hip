@@ -2,14 +2,16 @@
 //
 // Work decomposition.  One work-group per (batch*head, query block of BLK
 // rows, key range), launched so that the eight XCDs stream disjoint key ranges
-// of the same head (see the work-item decode below).  The work-group has
+// of the same head (see the work-item decode below).  Keys are processed in
+// tiles of 64 (a key block of BLK keys is BLK/64 tiles), so a 128-row query
+// block shares each K and V tile among four query slices.  The work-group has
 // 2 * BLK/32 wavefronts: wave w owns the 32-row query slice (w % (BLK/32)) and
-// the key half (w / (BLK/32)) of every key block, so each wave touches only
-// half of each K and V tile and two waves per SIMD stay resident (<= 256 VGPRs
+// the 32-key half (w / (BLK/32)) of every tile, so each wave touches only half
+// of each K and V tile and two waves per SIMD stay resident (<= 256 VGPRs
 // each).
 //
 // Per key block of the query block's ascending list:
-//   * K and V tiles (BLK x D each) go from global memory straight into LDS
+//   * K and V tiles (64 x D each) go from global memory straight into LDS
 //     (buffer_load ... lds, 1 KB per wave instruction, coalesced), with no
 //     VGPR staging.  LDS holds a ring of three K tiles and two V tiles: the K
 //     tile is needed one step before the V tile of the same block, and the
@@ -53,22 +55,25 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 template <int D, int BLK>
 struct AttnCfg {
+  static constexpr int KB = 64;               // keys per K/V tile
+  static constexpr int SUB = BLK / KB;        // tiles per key block (list entry)
   static constexpr int NQS = BLK / 32;        // 32-row query slices
-  static constexpr int NW = 2 * NQS;          // waves: (query slice, key half)
+  static constexpr int NW = 2 * NQS;          // waves: (query slice, key half of a tile)
   static constexpr int NT = 64 * NW;          // threads
-  static constexpr int KH = BLK / 2;          // keys per key half
+  static constexpr int KH = KB / 2;           // keys per key half
   static constexpr int KT = KH / 32;          // 32-key sub-tiles per wave and step
   static constexpr int DS = D / 16;           // MFMA k-steps over D
   static constexpr int DT = D / 32;           // 32-row d tiles of O^T
   static constexpr int RB = D * 2;            // bytes per K/V row
   static constexpr int CPR = D / 8;           // 16-byte chunks per row
   static constexpr int RPB = 256 / RB;        // rows per 256 bytes (one pass over the 64 LDS banks)
-  static constexpr int TILE = BLK * D;        // elements per K or V tile
+  static constexpr int TILE = KB * D;         // elements per K or V tile
   static constexpr int TILE_BYTES = TILE * 2;
   static constexpr int RPD = 1024 / RB;       // rows per direct-to-LDS wave load (64 lanes x 16 B)
   static constexpr int DPW = TILE_BYTES / 1024 / NW;  // direct loads per wave and tile
   static_assert(DPW * NW * 1024 == TILE_BYTES, "tile split over the waves");
-  static_assert(KT * 32 * 2 == BLK, "key halves");
+  static_assert(KT * 32 * 2 == KB, "key halves");
+  static_assert(SUB * KB == BLK, "whole tiles per key block");
 };
 
 // LDS tiles are stored unpadded (a direct-to-LDS load writes 1 KB contiguous
@@ -234,12 +239,13 @@ void attn_fwd_kernel(AttnArgs a) {
     cnt = __builtin_amdgcn_readfirstlane(c_hi) - pos_lo;
   }
 
-  // ---- block of list position pos_lo + j.  The entries are held 64 at a time
+  // ---- the key tiles of the item.  Tile j (KB keys) is tile j % SUB of the key
+  // block at list position pos_lo + j / SUB.  The entries are held 64 at a time
   // in a VGPR (lane i: entry lbase + i) and picked out with v_readlane, so the
-  // loop issues no memory load of its own except one batch load per 64 tiles.
-  // j >= cnt, and an entry outside [blk_lo, blk_hi) -- only possible in a list
-  // that is not ascending --, give -1: a tile that is loaded as zeros and fully
-  // masked.
+  // loop issues no memory load of its own except one batch load per 64
+  // entries.  j >= cnt * SUB, and an entry outside [blk_lo, blk_hi) -- only
+  // possible in a list that is not ascending --, give -1: a tile that is
+  // loaded as zeros and fully masked.
   int lreg = -1, lbase = 0;
   auto load_batch = [&](int base) {
     lbase = base;
@@ -250,14 +256,16 @@ void attn_fwd_kernel(AttnArgs a) {
       asm volatile("; list batch %0" ::"v"(lreg));
     }
   };
+  const int ntiles = cnt * C::SUB;
   auto fetch = [&](int j) -> int {
-    if (j >= cnt) return -1;
+    if (j >= ntiles) return -1;
+    const int e = j / C::SUB, sub = j % C::SUB;
     if constexpr (DENSE) {
-      return blk_lo + j;
+      return (blk_lo + e) * C::SUB + sub;
     } else {
-      if (j >= lbase + 64) load_batch(lbase + 64);
-      const int b = __builtin_amdgcn_readlane(lreg, j - lbase);
-      return (b >= blk_lo && b < blk_hi) ? b : -1;
+      if (e >= lbase + 64) load_batch(lbase + 64);
+      const int b = __builtin_amdgcn_readlane(lreg, e - lbase);
+      return (b >= blk_lo && b < blk_hi) ? b * C::SUB + sub : -1;
     }
   };
 
@@ -284,9 +292,12 @@ void attn_fwd_kernel(AttnArgs a) {
   }
   const uint16_t* const kbase = a.k + bh * a.lk * D;
   const uint16_t* const vbase = a.v + bh * a.lk * D;
-  const uint32_t last_bytes = (uint32_t)(a.lk - (int64_t)(a.n_k - 1) * BLK) * (uint32_t)C::RB;
-  auto tile_bytes = [&](int blk) -> uint32_t {
-    return blk < 0 ? 0u : (blk == a.n_k - 1 ? last_bytes : (uint32_t)C::TILE_BYTES);
+  // tiles are KB keys; the last one may be partial, and with SUB > 1 the last
+  // tiles of a partial key block may lie wholly past Lk (0 bytes)
+  const int n_kt = (int)((a.lk + C::KB - 1) / C::KB);
+  const uint32_t last_bytes = (uint32_t)(a.lk - (int64_t)(n_kt - 1) * C::KB) * (uint32_t)C::RB;
+  auto tile_bytes = [&](int kt) -> uint32_t {
+    return (kt < 0 || kt >= n_kt) ? 0u : (kt == n_kt - 1 ? last_bytes : (uint32_t)C::TILE_BYTES);
   };
   auto dma = [&](const uint16_t* base, int blk, uint16_t* slot, const uint32_t* off) {
     const i32x4 rs = raw_rsrc(base + (int64_t)(blk < 0 ? 0 : blk) * C::TILE, tile_bytes(blk));
@@ -338,8 +349,8 @@ void attn_fwd_kernel(AttnArgs a) {
 
   // keys >= Lk of a partial last block, and every key of a -1 tile, get -inf
   auto mask_tile = [&](f32x16* acc, int blk) {
-    const int64_t key0 = (int64_t)blk * BLK;
-    if (blk < 0 || key0 + BLK > a.lk) {
+    const int64_t key0 = (int64_t)blk * C::KB;
+    if (blk < 0 || key0 + C::KB > a.lk) {
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
@@ -388,7 +399,7 @@ void attn_fwd_kernel(AttnArgs a) {
       m_run = m_new;
     }
   };
-  auto needs_mask = [&](int blk) { return blk < 0 || (int64_t)blk * BLK + BLK > a.lk; };
+  auto needs_mask = [&](int blk) { return blk < 0 || (int64_t)blk * C::KB + C::KB > a.lk; };
 
   if (cnt > 0) {
     // ---- prologue.  The loads follow the order of the steady state (K(j+4)
@@ -522,7 +533,7 @@ void attn_fwd_kernel(AttnArgs a) {
           __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
         }
       }
-      if (t + 1 < cnt) {
+      if (t + 1 < ntiles) {
         if (needs_mask(b1)) {
           mask_tile(acc_n, b1);
           mx = tile_max(acc_n);
@@ -544,31 +555,30 @@ void attn_fwd_kernel(AttnArgs a) {
 
     while (true) {
       step(std::integral_constant<int, 0>{});
-      if (++t >= cnt) break;
+      if (++t >= ntiles) break;
       step(std::integral_constant<int, 1>{});
-      if (++t >= cnt) break;
+      if (++t >= ntiles) break;
       step(std::integral_constant<int, 2>{});
-      if (++t >= cnt) break;
+      if (++t >= ntiles) break;
       step(std::integral_constant<int, 3>{});
-      if (++t >= cnt) break;
+      if (++t >= ntiles) break;
       step(std::integral_constant<int, 4>{});
-      if (++t >= cnt) break;
+      if (++t >= ntiles) break;
       step(std::integral_constant<int, 5>{});
-      if (++t >= cnt) break;
+      if (++t >= ntiles) break;
     }
     wait_vmcnt<0>();  // loads past the end of the list still write LDS
   }
   __syncthreads();
 
   // ---- merge the two key halves of each query slice, then write O and lse.
-  // Key half 1 of slice qs leaves its 16 DT accumulators per lane in
-  // K slot qs*16 DT*256 bytes / TILE_BYTES (slots 0 and 1) and (m, l) in V slot 0.
+  // Key half 1 of slice qs leaves its 16 DT accumulators per lane in tile slot
+  // qs (K slots 0-2, then V slot 0) and (m, l) in V slot 1.
   l_run = half_swap_sum(l_run);  // both lane halves now hold the slice's partial sum
   constexpr int OB = 16 * C::DT * 64 * 4;  // bytes of one slice's accumulators
-  static_assert(C::NQS * OB <= 2 * C::TILE_BYTES, "merge buffer fits in K slots 0 and 1");
-  float* my_o = reinterpret_cast<float*>(reinterpret_cast<char*>((qs * OB) / C::TILE_BYTES == 0 ? ks0 : ks1) +
-                                         (qs * OB) % C::TILE_BYTES);
-  float* my_ml = reinterpret_cast<float*>(vs0) + qs * 2 * 64;
+  static_assert(OB == C::TILE_BYTES && C::NQS <= 4, "one slice's accumulators per tile slot");
+  float* my_o = reinterpret_cast<float*>(qs == 0 ? ks0 : qs == 1 ? ks1 : qs == 2 ? ks2 : vs0);
+  float* my_ml = reinterpret_cast<float*>(vs1) + qs * 2 * 64;
   if (kh == 1) {
     my_ml[0 * 64 + lane] = m_run;
     my_ml[1 * 64 + lane] = l_run;
