@@ -13,6 +13,7 @@ from .sparstar_oracle import (  # noqa: F401
     num_blocks,
     partition,
     pool,
+    retained_mass,
     retained_support,
     scale_densities,
     segment_blocks,
@@ -20,5 +21,6 @@ from .sparstar_oracle import (  # noqa: F401
     selectable_blocks,
     sparse_attention,
     token_mask,
+    token_topk_mass,
     topk_idx,
 )

@@ -250,3 +250,44 @@ def token_mask(lists: list[list[int]], lq: int, lk: int, b: int) -> np.ndarray:
             u0, u1 = block_token_range(j, lk, b)
             m[t0:t1, u0:u1] = True
     return m
+
+
+# --------------------------------------------------------------------------
+# Section 4 (Analysis): retained attention mass
+# --------------------------------------------------------------------------
+def _dense_probs(q: np.ndarray, k: np.ndarray, scale: float | None) -> np.ndarray:
+    """Row-wise softmax of scale * Q K^T over every key (float64)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    s = (1.0 / math.sqrt(q.shape[1])) if scale is None else float(scale)
+    z = s * (q @ k.T)
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    return p / p.sum(axis=1, keepdims=True)
+
+
+def retained_mass(q: np.ndarray, k: np.ndarray, lists: list[list[int]], b: int,
+                  scale: float | None = None) -> np.ndarray:
+    """Share of each query's dense softmax mass that falls on the keys its block
+    selection keeps: sum over u in the blocks of A_i (u < L_k) of
+    softmax_u(scale * q_t . k_u), the retained attention mass the paper's
+    analysis compares across selection strategies.  Returns [L_q]."""
+    p = _dense_probs(q, k, scale)
+    lq, lk = p.shape
+    out = np.zeros(lq, dtype=np.float64)
+    for i in range(num_blocks(lq, b)):
+        t0, t1 = block_token_range(i, lq, b)
+        cols = [u for j in lists[i] for u in range(*block_token_range(j, lk, b))]
+        if cols:
+            out[t0:t1] = p[t0:t1][:, cols].sum(axis=1)
+    return out
+
+
+def token_topk_mass(q: np.ndarray, k: np.ndarray, n_tokens: np.ndarray, scale: float | None = None) -> np.ndarray:
+    """The token-wise upper bound: for each query t, the largest softmax mass
+    any n_tokens[t] keys can hold, i.e. the sum of its n_tokens[t] largest
+    dense softmax weights.  Returns [L_q]."""
+    p = _dense_probs(q, k, scale)
+    srt = -np.sort(-p, axis=1)
+    n = np.asarray(n_tokens, dtype=np.int64)
+    return np.array([srt[t, : max(0, min(int(n[t]), p.shape[1]))].sum() for t in range(p.shape[0])])
+
