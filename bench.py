@@ -13,9 +13,10 @@ divided by the step time.  `roofline` reports the sparse forward call against
 the bf16 MFMA peak, timed with HIP events on the stream it runs on; `traffic`
 comes from the committed rocprofv3 counter summary when it was taken on the
 current kernel source.  Also reported: the in-house dense forward on the same
-shape, the density sweep (per-head budgets around 10 / 25 / 50%), the
-five-scale clip pyramid, and the float64 CPU oracle timed on a bounded sample
-(`cpu_baseline`).
+shape, the retained attention mass of the selection against the token-wise
+top-K bound (Section 4's diagnostic, on the synthetic inputs), the density sweep
+(per-head budgets around 10 / 25 / 50%), the five-scale clip pyramid, and the
+float64 CPU oracle timed on a bounded sample (`cpu_baseline`).
 """
 from __future__ import annotations
 
@@ -177,6 +178,51 @@ class Runner:
         return 4.0 * B * H * Lq * Lk * D
 
 
+MASS_DENSITIES = (0.25, 0.30, 0.50)
+MASS_ROWS = 8
+
+
+def attention_mass(r: "Runner", S, torch) -> dict:
+    """Section 4's diagnostic on the bench inputs: the dense softmax mass each
+    query's block selection keeps, exp(lse_sparse - lse_dense) for every query,
+    and, on MASS_ROWS sampled queries per head, the token-wise bound (the mass
+    of the same number of best single keys)."""
+    B, H, Lq, Lk, D = r.shape
+    b = r.w.block
+    dev = r.q.device
+    _, lse_all = S.sparstar_dense_attn_fwd(r.q, r.k, r.v, b, workspace=r.aws)
+    rows = [int(x) for x in np.linspace(0, Lq - 1, MASS_ROWS)]
+    ws = torch.empty(S.sparstar_token_topk_workspace_bytes(B, H, Lk, len(rows)), dtype=torch.uint8, device=dev)
+    res, mass_ms = [], []
+    for rho in MASS_DENSITIES:
+        stride = S.sparstar_kv_stride(H, Lk, b, rho, r.keep)
+        num, idx = S.sparstar_score_blocks(r.q, r.k, b, rho, r.keep, kv_stride=stride, workspace=r.ws)
+        _, lse_sel = S.sparstar_sparse_attn_fwd(r.q, r.k, r.v, num, idx, b, workspace=r.aws)
+        e0, e1 = r.ev(), r.ev()
+        e0.record()
+        mass = S.sparstar_retained_mass(lse_sel, lse_all)
+        e1.record()
+        torch.cuda.synchronize()
+        mass_ms.append(e0.elapsed_time(e1))
+        nb = num.cpu().numpy()
+        ix = idx.cpu().numpy()
+        n_tok = np.zeros((B, H, len(rows)), dtype=np.int32)
+        for h in range(H):
+            for j, t in enumerate(rows):
+                lst = ix[0, h, t // b, : nb[0, h, t // b]]
+                n_tok[0, h, j] = int(np.sum(np.minimum((lst + 1) * b, Lk) - lst * b))
+        bound = S.sparstar_token_topk_mass(r.q, r.k, rows, torch.from_numpy(n_tok).to(dev), lse_all, workspace=ws)
+        m = mass.cpu().numpy().astype(np.float64)
+        bd = bound.cpu().numpy().astype(np.float64)
+        ms_rows = m[:, :, rows]
+        res.append({"density": rho, "block_mean": float(m.mean()), "block_min": float(m.min()),
+                    "block_mean_sampled": float(ms_rows.mean()), "token_bound_mean_sampled": float(bd.mean()),
+                    "gap_sampled": float((bd - ms_rows).mean())})
+        del num, idx, lse_sel, mass
+    return {"rows_sampled_per_head": len(rows), "by_density": res, "mass_kernel_ms": float(np.median(mass_ms)),
+            "data": "synthetic (no trained model): absolute values are not the paper's"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -189,6 +235,7 @@ def main() -> int:
     ap.add_argument("--no-pyramid", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache selector timing")
     ap.add_argument("--no-b128", action="store_true", help="skip the 720p run at block size 128")
+    ap.add_argument("--no-mass", action="store_true", help="skip the retained-attention-mass diagnostic")
     ap.add_argument("--gen-workers", type=int, default=None,
                     help="input-generation processes (1 = in-process; use 1 under a profiler)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -337,6 +384,13 @@ def main() -> int:
             "speedup_sparse_fwd_only": dense_ms / att_avg,
         }
         log(f"dense {dense_ms:.2f} ms -> speedup {dense_ms / ms_step:.2f}x (step), {dense_ms / att_avg:.2f}x (fwd)")
+
+    if not args.no_mass:
+        log("retained attention mass (selection vs token-wise top-K bound)")
+        out["attention_mass"] = attention_mass(r, S, torch)
+        for row in out["attention_mass"]["by_density"]:
+            log(f"  rho={row['density']}: block top-k keeps {row['block_mean']:.4f} of the dense mass "
+                f"(sampled rows {row['block_mean_sampled']:.4f}, token bound {row['token_bound_mean_sampled']:.4f})")
 
     if b128_data is not None:
         log("720p at the paper's deployed block size 128")

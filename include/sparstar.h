@@ -202,6 +202,54 @@ int sparstar_clip_keep_ranges(int clip, sparstar_range text, sparstar_range ref,
 int sparstar_scale_densities(const int64_t* scale_lq, int n_scales, const double* finest_rho, int n_finest,
                              double* rho_out);
 
+/*
+ * Retained attention mass (Section 4, the analysis of how much dense softmax
+ * mass a selection keeps): for every query t,
+ *   mass_t = sum over the selected keys u of softmax_u(s * q_t . k_u)
+ *          = exp(lse_sel_t - lse_all_t),
+ * where lse_sel is the log-sum-exp written by sparstar_sparse_attn_fwd and
+ * lse_all the one written by sparstar_dense_attn_fwd on the same Q, K and
+ * softmax scale.  A row with lse_sel = -inf (an empty list) gets 0.
+ *   lse_sel, lse_all   device fp32 [n], 4-byte aligned
+ *   mass               device fp32 out [n]; may be the same buffer as lse_sel
+ * Returns SPARSTAR_OK, or SPARSTAR_ERR_INVALID_ARG for n < 0 or a NULL pointer
+ * with n > 0.
+ */
+int sparstar_retained_mass(const float* lse_sel, const float* lse_all, int64_t n, float* mass, void* stream);
+
+/* Upper bound on the sampled query rows of sparstar_token_topk_mass. */
+#define SPARSTAR_MAX_MASS_ROWS 16
+
+/*
+ * Bytes of device scratch sparstar_token_topk_mass needs: the fp32 logits of
+ * the sampled rows against every key, [B, H, n_rows, Lk].  0 for invalid sizes.
+ */
+size_t sparstar_token_topk_workspace_bytes(int B, int H, int64_t Lk, int n_rows);
+
+/*
+ * Token-wise upper bound of the retained mass (Section 4): for each (b, h) and
+ * each sampled query position t = rows[r], the largest dense softmax mass any
+ * n = n_tokens[b,h,r] keys can hold, i.e. the sum of the n largest weights
+ *   exp(s * q_t . k_u - lse_all[b,h,t])   over u in [0, Lk).
+ * The logits are recomputed in fp32 from the bf16 inputs; equal logits at the
+ * n-th place fill the remaining places one weight each.
+ *   q, k, B, H, Lq, Lk, D, softmax_scale   as for sparstar_dense_attn_fwd
+ *                   (Lq >= 1, B * H <= 65535)
+ *   rows, n_rows    HOST int64 [n_rows], 1 <= n_rows <= SPARSTAR_MAX_MASS_ROWS:
+ *                   query positions in [0, Lq), the same for every (b, h)
+ *   n_tokens        device int32 [B, H, n_rows]; each value is clamped to [0, Lk]
+ *   lse_all         device fp32 [B, H, Lq], the dense log-sum-exp on the same
+ *                   inputs and scale (sparstar_dense_attn_fwd)
+ *   mass            device fp32 out [B, H, n_rows]
+ *   workspace       device scratch of >= sparstar_token_topk_workspace_bytes(...)
+ *                   bytes, 4-byte aligned, garbage afterwards
+ * Returns SPARSTAR_OK or a negative code as for the other calls.
+ */
+int sparstar_token_topk_mass(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
+                             const int64_t* rows, int n_rows, const int32_t* n_tokens, const float* lse_all,
+                             float softmax_scale, float* mass, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
 /* Message for the last non-OK return on this thread ("" if none). */
 const char* sparstar_last_error(void);
 

@@ -329,3 +329,79 @@ extern "C" int sparstar_dense_attn_fwd(const void* q, const void* k, const void*
   return attn_common(q, k, v, B, H, Lq, Lk, D, block_size, nullptr, nullptr, 0, softmax_scale, o, lse, workspace,
                      workspace_bytes, stream, true);
 }
+
+extern "C" int sparstar_retained_mass(const float* lse_sel, const float* lse_all, int64_t n, float* mass,
+                                      void* stream) {
+  if (n < 0) return fail(SPARSTAR_ERR_INVALID_ARG, "n must be >= 0 (got %lld)", (long long)n);
+  if (n > 0 && (!lse_sel || !lse_all || !mass))
+    return fail(SPARSTAR_ERR_INVALID_ARG, "lse_sel, lse_all and mass must be non-null");
+  const uintptr_t mis = reinterpret_cast<uintptr_t>(lse_sel) | reinterpret_cast<uintptr_t>(lse_all) |
+                        reinterpret_cast<uintptr_t>(mass);
+  if (mis & 3u) return fail(SPARSTAR_ERR_INVALID_ARG, "lse_sel, lse_all and mass must be 4-byte aligned");
+  hipError_t e = sparstar::launch_retained_mass(lse_sel, lse_all, n, mass, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "retained-mass launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+static_assert(sparstar::kTopkMaxRows == SPARSTAR_MAX_MASS_ROWS, "sampled-row limit");
+
+static int check_topk_sizes(int B, int H, int64_t Lk, int n_rows) {
+  if (B < 1 || H < 1 || int64_t(B) * H > 65535)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "need B, H >= 1 and B * H <= 65535 (got B=%d, H=%d)", B, H);
+  if (Lk < 1 || Lk > (int64_t(1) << 30)) return fail(SPARSTAR_ERR_INVALID_ARG, "Lk must be in [1, 2^30]");
+  if (n_rows < 1 || n_rows > SPARSTAR_MAX_MASS_ROWS)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "n_rows must be in [1, %d] (got %d)", SPARSTAR_MAX_MASS_ROWS, n_rows);
+  if (int64_t(B) * H * n_rows * Lk > (int64_t(1) << 40)) return fail(SPARSTAR_ERR_INVALID_ARG, "too many logits");
+  return SPARSTAR_OK;
+}
+
+extern "C" size_t sparstar_token_topk_workspace_bytes(int B, int H, int64_t Lk, int n_rows) {
+  if (check_topk_sizes(B, H, Lk, n_rows) != SPARSTAR_OK) return 0;
+  return size_t(int64_t(B) * H * n_rows * Lk) * sizeof(float);
+}
+
+extern "C" int sparstar_token_topk_mass(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
+                                        const int64_t* rows, int n_rows, const int32_t* n_tokens,
+                                        const float* lse_all, float softmax_scale, float* mass, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  using namespace sparstar;
+  if (int rc = check_topk_sizes(B, H, Lk, n_rows)) return rc;
+  if (Lq < 1 || Lq > (int64_t(1) << 30)) return fail(SPARSTAR_ERR_INVALID_ARG, "Lq must be in [1, 2^30]");
+  if (D != 64 && D != 128) return fail(SPARSTAR_ERR_UNSUPPORTED, "head dim %d not supported (64 or 128)", D);
+  if (int64_t(B) * H * std::max(Lq, Lk) * D > (int64_t(1) << 46))
+    return fail(SPARSTAR_ERR_INVALID_ARG, "tensor too large");
+  if (!q || !k || !rows || !n_tokens || !lse_all || !mass)
+    return fail(SPARSTAR_ERR_INVALID_ARG, "q, k, rows, n_tokens, lse_all and mass must be non-null");
+  if (!aligned16(q) || !aligned16(k)) return fail(SPARSTAR_ERR_INVALID_ARG, "q and k must be 16-byte aligned");
+  const uintptr_t mis = reinterpret_cast<uintptr_t>(n_tokens) | reinterpret_cast<uintptr_t>(lse_all) |
+                        reinterpret_cast<uintptr_t>(mass);
+  if (mis & 3u) return fail(SPARSTAR_ERR_INVALID_ARG, "n_tokens, lse_all and mass must be 4-byte aligned");
+  for (int r = 0; r < n_rows; ++r)
+    if (rows[r] < 0 || rows[r] >= Lq)
+      return fail(SPARSTAR_ERR_INVALID_ARG, "rows[%d] = %lld is outside [0, Lq=%lld)", r, (long long)rows[r],
+                  (long long)Lq);
+  if (!(softmax_scale == softmax_scale) || isinf(softmax_scale))
+    return fail(SPARSTAR_ERR_INVALID_ARG, "softmax_scale must be finite");
+  const size_t need = sparstar_token_topk_workspace_bytes(B, H, Lk, n_rows);
+  if (!workspace) return fail(SPARSTAR_ERR_WORKSPACE, "workspace is null");
+  if (reinterpret_cast<uintptr_t>(workspace) & 3u)
+    return fail(SPARSTAR_ERR_WORKSPACE, "workspace must be 4-byte aligned");
+  if (workspace_bytes < need)
+    return fail(SPARSTAR_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
+  TopkArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.n_tokens = n_tokens;
+  a.lse_all = lse_all;
+  a.scores = static_cast<float*>(workspace);
+  a.mass = mass;
+  a.lq = Lq;
+  a.lk = Lk;
+  a.bh = int64_t(B) * H;
+  a.n_rows = n_rows;
+  for (int r = 0; r < n_rows; ++r) a.rows[r] = rows[r];
+  a.scale = float(softmax_scale > 0.f ? double(softmax_scale) : 1.0 / sqrt(double(D)));
+  hipError_t e = launch_topk_mass(a, D, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "token top-n mass launch: %s", hipGetErrorString(e));
+  return ok();
+}

@@ -76,9 +76,30 @@ constexpr int kSplits = 16;
 // Bytes of attention workspace for the key-range split (0 when it is not used).
 size_t attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block);
 
+// Token-wise top-n mass (the upper bound of the retained-mass analysis) for a
+// few sampled query rows per head.
+constexpr int kTopkMaxRows = 16;
+
+struct TopkArgs {
+  const uint16_t* q;        // [BH, Lq, D] bf16
+  const uint16_t* k;        // [BH, Lk, D] bf16
+  const int32_t* n_tokens;  // [BH, n_rows]
+  const float* lse_all;     // [BH, Lq] dense log-sum-exp
+  float* scores;            // [BH, n_rows, Lk] fp32 logits (workspace)
+  float* mass;              // [BH, n_rows]
+  int64_t lq, lk;
+  int64_t bh;
+  int n_rows;
+  int64_t rows[kTopkMaxRows];  // sampled query positions, shared by every head
+  float scale;
+};
+
 hipError_t launch_pool(const PoolArgs& a, int d, int block, hipStream_t stream);
 hipError_t launch_score(const ScoreArgs& a, int d, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_attn(const AttnArgs& a, int d, int block, bool dense, hipStream_t stream);
+hipError_t launch_retained_mass(const float* lse_sel, const float* lse_all, int64_t n, float* mass,
+                                hipStream_t stream);
+hipError_t launch_topk_mass(const TopkArgs& a, int d, hipStream_t stream);
 
 }  // namespace sparstar

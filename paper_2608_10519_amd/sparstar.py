@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libsparstar.so")
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 MAX_KEEP_RANGES = 8
+MAX_MASS_ROWS = 16
 
 _lib = None
 
@@ -59,6 +60,13 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.sparstar_dense_attn_fwd.argtypes = [c_p, c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_f, c_p, c_p, c_p,
                                             c_sz, c_p]
     lib.sparstar_dense_attn_fwd.restype = c_i
+    lib.sparstar_retained_mass.argtypes = [c_p, c_p, c_i64, c_p, c_p]
+    lib.sparstar_retained_mass.restype = c_i
+    lib.sparstar_token_topk_workspace_bytes.argtypes = [c_i, c_i, c_i64, c_i]
+    lib.sparstar_token_topk_workspace_bytes.restype = c_sz
+    lib.sparstar_token_topk_mass.argtypes = [c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, ctypes.POINTER(ctypes.c_int64),
+                                             c_i, c_p, c_p, c_f, c_p, c_p, c_sz, c_p]
+    lib.sparstar_token_topk_mass.restype = c_i
     lib.sparstar_last_error.argtypes = []
     lib.sparstar_last_error.restype = ctypes.c_char_p
     lib.sparstar_clip_keep_ranges.argtypes = [c_i, Range, Range, c_rp, c_i]
@@ -226,3 +234,47 @@ def sparstar_dense_attn_fwd(q, k, v, block_size: int = 64, softmax_scale: float 
                                         lse.data_ptr() if lse is not None else None, wp, wn, _stream())
     _check("sparstar_dense_attn_fwd", rc)
     return o, lse
+
+
+def sparstar_retained_mass(lse_sel: torch.Tensor, lse_all: torch.Tensor, *, out: torch.Tensor | None = None):
+    """exp(lse_sel - lse_all) elementwise (0 where lse_sel is -inf): the share of
+    each query's dense softmax mass its block selection keeps."""
+    for t, name in ((lse_sel, "lse_sel"), (lse_all, "lse_all")):
+        if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous fp32 tensor on the GPU")
+    if lse_sel.shape != lse_all.shape:
+        raise ValueError("lse_sel and lse_all differ in shape")
+    mass = torch.empty_like(lse_sel) if out is None else out
+    rc = load().sparstar_retained_mass(lse_sel.data_ptr(), lse_all.data_ptr(), lse_sel.numel(), mass.data_ptr(),
+                                       _stream())
+    _check("sparstar_retained_mass", rc)
+    return mass
+
+
+def sparstar_token_topk_workspace_bytes(B: int, H: int, Lk: int, n_rows: int) -> int:
+    return int(load().sparstar_token_topk_workspace_bytes(B, H, Lk, n_rows))
+
+
+def sparstar_token_topk_mass(q: torch.Tensor, k: torch.Tensor, rows: Sequence[int], n_tokens: torch.Tensor,
+                             lse_all: torch.Tensor, softmax_scale: float = 0.0, *,
+                             workspace: torch.Tensor | None = None):
+    """Sum of the n_tokens[b,h,r] largest dense softmax weights of query rows[r]:
+    the token-wise upper bound of the retained mass.  Returns [B, H, len(rows)] fp32."""
+    B, H, Lq, D = _bhld(q, "q")
+    _, _, Lk, _ = _bhld(k, "k")
+    n = len(rows)
+    if n_tokens.dtype != torch.int32 or not n_tokens.is_contiguous() or tuple(n_tokens.shape) != (B, H, n):
+        raise ValueError("n_tokens must be a contiguous int32 tensor [B, H, len(rows)]")
+    if lse_all.dtype != torch.float32 or not lse_all.is_contiguous() or tuple(lse_all.shape) != (B, H, Lq):
+        raise ValueError("lse_all must be a contiguous fp32 tensor [B, H, Lq]")
+    r = (ctypes.c_int64 * max(n, 1))(*[int(x) for x in rows])
+    need = sparstar_token_topk_workspace_bytes(B, H, Lk, n)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    mass = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
+    rc = load().sparstar_token_topk_mass(q.data_ptr(), k.data_ptr(), B, H, Lq, Lk, D, r, n, n_tokens.data_ptr(),
+                                         lse_all.data_ptr(), float(softmax_scale), mass.data_ptr(),
+                                         workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                         _stream())
+    _check("sparstar_token_topk_mass", rc)
+    return mass

@@ -164,3 +164,60 @@ def test_last_error_is_cleared_by_success(lib):
     assert S.last_error()
     assert S.sparstar_kv_stride(2, 1152, 64, 0.25, [(512, 640)]) == 6
     assert S.last_error() == ""
+
+
+def test_token_topk_workspace_bytes(lib):
+    # fp32 logits [B, H, n_rows, Lk]
+    assert S.sparstar_token_topk_workspace_bytes(1, 24, 144_512, 8) == 24 * 8 * 144_512 * 4
+    assert S.sparstar_token_topk_workspace_bytes(1, 2, 100, 0) == 0
+    assert S.sparstar_token_topk_workspace_bytes(1, 2, 100, S.MAX_MASS_ROWS + 1) == 0
+    assert S.sparstar_token_topk_workspace_bytes(300, 300, 100, 1) == 0  # B * H above 65535
+
+
+def _topk(lib, **over):
+    import ctypes
+
+    a = dict(q=FAKE, k=FAKE, B=1, H=2, Lq=512, Lk=1152, D=64, rows=[0, 5, 511], ntok=FAKE, lse=FAKE, scale=0.0,
+             mass=FAKE, ws=FAKE, ws_bytes=1 << 30)
+    a.update(over)
+    rows = a["rows"]
+    arr = (ctypes.c_int64 * max(1, len(rows)))(*rows) if rows is not None else None
+    return lib.sparstar_token_topk_mass(a["q"], a["k"], a["B"], a["H"], a["Lq"], a["Lk"], a["D"], arr,
+                                        len(rows) if rows is not None else 1, a["ntok"], a["lse"], a["scale"],
+                                        a["mass"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("over,code,msg", [
+    (dict(q=None), S.ERR_INVALID_ARG, "non-null"),
+    (dict(rows=None), S.ERR_INVALID_ARG, "non-null"),
+    (dict(ntok=None), S.ERR_INVALID_ARG, "non-null"),
+    (dict(k=FAKE + 8), S.ERR_INVALID_ARG, "16-byte"),
+    (dict(lse=FAKE + 2), S.ERR_INVALID_ARG, "4-byte"),
+    (dict(rows=[0, 512]), S.ERR_INVALID_ARG, "outside"),
+    (dict(rows=[-1]), S.ERR_INVALID_ARG, "outside"),
+    (dict(rows=[]), S.ERR_INVALID_ARG, "n_rows"),
+    (dict(rows=list(range(17))), S.ERR_INVALID_ARG, "n_rows"),
+    (dict(D=96), S.ERR_UNSUPPORTED, "head dim"),
+    (dict(Lq=0), S.ERR_INVALID_ARG, "Lq"),
+    (dict(scale=float("nan")), S.ERR_INVALID_ARG, "finite"),
+    (dict(ws=None), S.ERR_WORKSPACE, "null"),
+    (dict(ws_bytes=100), S.ERR_WORKSPACE, "required"),
+])
+def test_token_topk_mass_rejects_invalid_arguments(lib, over, code, msg):
+    assert _topk(lib, **over) == code
+    assert msg in S.last_error()
+
+
+@pytest.mark.parametrize("args,msg", [
+    ((FAKE, FAKE, -1, FAKE), ">= 0"),
+    ((None, FAKE, 4, FAKE), "non-null"),
+    ((FAKE, FAKE, 4, FAKE + 2), "4-byte"),
+])
+def test_retained_mass_rejects_invalid_arguments(lib, args, msg):
+    assert lib.sparstar_retained_mass(*args, None) == S.ERR_INVALID_ARG
+    assert msg in S.last_error()
+
+
+def test_retained_mass_empty_is_noop(lib):
+    # n = 0 launches nothing, so it succeeds without a device
+    assert lib.sparstar_retained_mass(None, None, 0, None, None) == S.OK
