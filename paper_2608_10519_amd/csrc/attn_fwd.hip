@@ -135,18 +135,48 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)p);
 }
 
-// One wave-wide direct-to-LDS load: lane l copies 16 bytes from buffer offset
-// voff to LDS byte m0 + 16 l.  Written as inline assembly so that the compiler
-// does not order every later LDS read behind it; each caller waits for these
+// Direct-to-LDS loads: lane l of a wave-wide load copies 16 bytes from
+// buffer offset voff (+ the instruction offset) to LDS byte m0 (+ the same
+// instruction offset) + 16 l.  Written as inline assembly so that the compiler
+// does not order every later LDS read behind them; each caller waits for these
 // loads explicitly (vmcnt) before a barrier makes the tile visible.
-__device__ __forceinline__ void dma16(uint32_t m0, uint32_t voff, i32x4 rsrc) {
-  asm volatile(
-      "s_mov_b32 m0, %0\n\t"
-      "s_nop 0\n\t"
-      "buffer_load_dwordx4 %1, %2, 0 offen lds"
-      :
-      : "s"(m0), "v"(voff), "s"(rsrc)
-      : "memory", "m0");
+//
+// A wave's share of one tile: N wave-wide loads after a single M0 write.  The
+// instruction offset moves the LDS destination and the memory address alike,
+// so load i goes to LDS m0 + 1024 i + 16 l and reads voff[i] + 1024 i (the
+// callers pass voff[i] already reduced by 1024 i).
+template <int N>
+__device__ __forceinline__ void dma_tile(uint32_t m0, const uint32_t* voff, i32x4 rsrc) {
+  static_assert(N == 1 || N == 2 || N == 4, "loads per wave and tile");
+  if constexpr (N == 1) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(m0), "v"(voff[0]), "s"(rsrc)
+        : "memory", "m0");
+  } else if constexpr (N == 2) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %3, 0 offen lds\n\t"
+        "buffer_load_dwordx4 %2, %3, 0 offen offset:1024 lds"
+        :
+        : "s"(m0), "v"(voff[0]), "v"(voff[1]), "s"(rsrc)
+        : "memory", "m0");
+  } else {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %5, 0 offen lds\n\t"
+        "buffer_load_dwordx4 %2, %5, 0 offen offset:1024 lds\n\t"
+        "buffer_load_dwordx4 %3, %5, 0 offen offset:2048 lds\n\t"
+        "buffer_load_dwordx4 %4, %5, 0 offen offset:3072 lds"
+        :
+        : "s"(m0), "v"(voff[0]), "v"(voff[1]), "v"(voff[2]), "v"(voff[3]), "s"(rsrc)
+        : "memory", "m0");
+  }
 }
 
 // s_waitcnt with only the vector-memory counter constrained (<= n outstanding)
@@ -282,13 +312,14 @@ void attn_fwd_kernel(AttnArgs a) {
   // chunk l % CPR of row RPD (DPW w + i) + l / CPR, and so reads the logical
   // chunk that the XOR permutation puts there.  Each tile gets its own
   // descriptor (records = bytes of the tile that exist), so rows past Lk and
-  // the tiles past the end of the list arrive as zeros.
+  // the tiles past the end of the list arrive as zeros.  The offsets are kept
+  // minus 1024 i, the instruction offset of load i.
   uint32_t kdma[C::DPW], vdma[C::DPW];
 #pragma unroll
   for (int i = 0; i < C::DPW; ++i) {
     const int row = C::RPD * (C::DPW * wave + i) + lane / C::CPR, pos = lane % C::CPR;
-    kdma[i] = (uint32_t)(row * C::RB + 16 * (pos ^ k_swz<D, BLK>(row)));
-    vdma[i] = (uint32_t)(row * C::RB + 16 * (pos ^ v_swz<D, BLK>(row)));
+    kdma[i] = (uint32_t)(row * C::RB + 16 * (pos ^ k_swz<D, BLK>(row)) - 1024 * i);
+    vdma[i] = (uint32_t)(row * C::RB + 16 * (pos ^ v_swz<D, BLK>(row)) - 1024 * i);
   }
   const uint16_t* const kbase = a.k + bh * a.lk * D;
   const uint16_t* const vbase = a.v + bh * a.lk * D;
@@ -301,9 +332,7 @@ void attn_fwd_kernel(AttnArgs a) {
   };
   auto dma = [&](const uint16_t* base, int blk, uint16_t* slot, const uint32_t* off) {
     const i32x4 rs = raw_rsrc(base + (int64_t)(blk < 0 ? 0 : blk) * C::TILE, tile_bytes(blk));
-    const uint32_t m0 = lds_addr(slot) + (uint32_t)(C::DPW * wave) * 1024u;
-#pragma unroll
-    for (int i = 0; i < C::DPW; ++i) dma16(m0 + 1024u * i, off[i], rs);
+    dma_tile<C::DPW>(lds_addr(slot) + (uint32_t)(C::DPW * wave) * 1024u, off, rs);
   };
 
   // ---- per-lane LDS read offsets (bytes within a tile)
