@@ -38,6 +38,13 @@ def _ws_views(ws, B, H, n_q, n_k, D):
     return f[:qn].view(B, H, n_q, D), f[off_k: off_k + B * H * n_k * D].view(B, H, n_k, D)
 
 
+def _times_pow2(bits: np.ndarray, e: int) -> np.ndarray:
+    """bf16 bit patterns scaled by 2^e exactly (finite, normal values)."""
+    from synthetic.workloads import bf16_bits
+
+    return bf16_bits((bf16_to_f64(bits) * 2.0 ** e).astype(np.float32))
+
+
 def _run_selector(lib, w: Workload, q, k, keep, budget, with_scores=True):
     import torch
 
@@ -64,6 +71,9 @@ SELECTOR_CASES = [
                                     heads=2, seed=9, density=0.4), 2),
     ("many-tiles", TINY.with_(name="r4", head_dim=128, lq=64 * 70 + 5, l_ref=64 * 60 + 9, l_text=200, heads=2,
                               seed=10, aligned=5, density=0.3), 2),
+    # more than 3584 key blocks: the rows no longer fit the select kernel's LDS cache
+    ("long-rows", TINY.with_(name="r5", heads=1, lq=200, l_ref=64 * 3650 + 17, l_text=128, seed=11,
+                             density=0.2), 2),
 ]
 
 
@@ -71,6 +81,10 @@ SELECTOR_CASES = [
 def test_selector_matches_oracle(gpu_lib, name, w, clip):
     _say(f"[selector] {name}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk} clip={clip}")
     qb_, kb_, _ = generate(w)
+    if name == "long-rows":
+        # 3,600 candidates per row crowd the scores together; x8 (exact in bf16)
+        # spreads them so that some rows have a clear top-k boundary
+        qb_, kb_ = _times_pow2(qb_, 3), _times_pow2(kb_, 3)
     keep = keep_ranges(w, clip)
     num, idx, scores, qbar, kbar = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, w.density)
     lists = lists_from_device(num, idx)
