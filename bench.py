@@ -236,6 +236,7 @@ def main() -> int:
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache selector timing")
     ap.add_argument("--no-b128", action="store_true", help="skip the 720p run at block size 128")
     ap.add_argument("--no-mass", action="store_true", help="skip the retained-attention-mass diagnostic")
+    ap.add_argument("--no-graph", action="store_true", help="skip the graph-captured step timing")
     ap.add_argument("--gen-workers", type=int, default=None,
                     help="input-generation processes (1 = in-process; use 1 under a profiler)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -372,6 +373,33 @@ def main() -> int:
         out["breakdown_ms"]["score_blocks_cold_min"] = float(np.min(cold))
         log(f"selector from cold caches: median {np.median(cold):.3f} ms "
             f"({read_bytes / (np.median(cold) * 1e-3) / 1e12:.2f} TB/s of Q+K over the whole selector call)")
+
+    if not args.no_graph:
+        # the same step captured once in a HIP graph (both calls only launch
+        # kernels on the stream) and replayed K times
+        log("graph-captured step")
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            r.score()
+            r.sparse()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                r.score()
+                r.sparse()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        g_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        out["graph"] = {"ms_per_step": g_ms, "speedup_vs_eager": ms_step / g_ms}
+        log(f"graph step {g_ms:.3f} ms (eager {ms_step:.3f} ms)")
+        del graph
 
     dense_ms = None
     if not args.no_dense:
