@@ -217,6 +217,25 @@ def test_sparse_attention_matches_oracle(gpu_lib, name, w, sharp, split):
     _say(f"[attn] {name}: max |dO| = {err:.2e}")
 
 
+@pytest.mark.parametrize("name,w", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
+def test_softmax_weights_sum_to_one(gpu_lib, name, w):
+    """Invariant of Eq. 7: with the GPU's lse and the oracle's float64 logits, the
+    weights exp(s q_t . k_u - lse_t) over the visible keys of each query sum to
+    one, within exp(LSE_ABS) - 1 (each lse is within LSE_ABS of the exact value)."""
+    rng = np.random.default_rng(zlib.crc32(name.encode()) % 1000 + 7)
+    lists_h = _random_lists(w, rng)
+    _say(f"[attn] softmax sums {name}")
+    _, lg, _, _, (qb_, kb_, _) = _attn_case(gpu_lib, w, lists_h)
+    tol = math.exp(LSE_ABS) - 1
+    for h in range(w.heads):
+        q, k = bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h])
+        z = (q @ k.T) / math.sqrt(w.head_dim)
+        vis = O.token_mask(lists_h[h], w.lq, w.lk, w.block)
+        tot = np.where(vis, np.exp(z - lg[0, h][:, None]), 0.0).sum(axis=1)
+        err = np.abs(tot - 1.0)
+        assert err.max() <= tol, f"{name} head {h}: max |sum - 1| = {err.max():.3e}"
+
+
 def test_end_to_end_tiny_against_oracle(gpu_lib):
     """Selector + sparse forward on the tiny workload, each stage against the oracle."""
     import torch
