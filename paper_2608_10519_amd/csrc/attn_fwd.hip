@@ -58,9 +58,13 @@ struct AttnCfg {
   static constexpr int KB = 64;               // keys per K/V tile
   static constexpr int SUB = BLK / KB;        // tiles per key block (list entry)
   static constexpr int NQS = BLK / 32;        // 32-row query slices
-  static constexpr int NW = 2 * NQS;          // waves: (query slice, key half of a tile)
+  // key parts per tile: with 64-row blocks two waves share a slice, each
+  // taking one 32-key half of every tile; with 128-row blocks one wave takes
+  // the whole tile, so the four waves of a work-group never split a key
+  static constexpr int KSP = BLK == 128 ? 1 : 2;
+  static constexpr int NW = KSP * NQS;        // waves: (query slice, key part of a tile)
   static constexpr int NT = 64 * NW;          // threads
-  static constexpr int KH = KB / 2;           // keys per key half
+  static constexpr int KH = KB / KSP;         // keys per key part
   static constexpr int KT = KH / 32;          // 32-key sub-tiles per wave and step
   static constexpr int DS = D / 16;           // MFMA k-steps over D
   static constexpr int DT = D / 32;           // 32-row d tiles of O^T
@@ -72,7 +76,7 @@ struct AttnCfg {
   static constexpr int RPD = 1024 / RB;       // rows per direct-to-LDS wave load (64 lanes x 16 B)
   static constexpr int DPW = TILE_BYTES / 1024 / NW;  // direct loads per wave and tile
   static_assert(DPW * NW * 1024 == TILE_BYTES, "tile split over the waves");
-  static_assert(KT * 32 * 2 == KB, "key halves");
+  static_assert(KT * 32 * KSP == KB, "key parts");
   static_assert(SUB * KB == BLK, "whole tiles per key block");
 };
 
@@ -312,14 +316,16 @@ void attn_fwd_kernel(AttnArgs a) {
   // chunk l % CPR of row RPD (DPW w + i) + l / CPR, and so reads the logical
   // chunk that the XOR permutation puts there.  Each tile gets its own
   // descriptor (records = bytes of the tile that exist), so rows past Lk and
-  // the tiles past the end of the list arrive as zeros.  The offsets are kept
-  // minus 1024 i, the instruction offset of load i.
-  uint32_t kdma[C::DPW], vdma[C::DPW];
-#pragma unroll
-  for (int i = 0; i < C::DPW; ++i) {
-    const int row = C::RPD * (C::DPW * wave + i) + lane / C::CPR, pos = lane % C::CPR;
-    kdma[i] = (uint32_t)(row * C::RB + 16 * (pos ^ k_swz<D, BLK>(row)) - 1024 * i);
-    vdma[i] = (uint32_t)(row * C::RB + 16 * (pos ^ v_swz<D, BLK>(row)) - 1024 * i);
+  // the tiles past the end of the list arrive as zeros.  Load i adds 1024 i
+  // bytes (RPD rows) to both sides, which moves the K permutation by 4 chunks
+  // and leaves the V permutation unchanged; with the instruction offset taking
+  // the 1024 i, the per-lane offset of load i is kdma ^ 64 i for K and vdma for
+  // V (the identity holds for every configuration built).
+  uint32_t kdma, vdma;
+  {
+    const int row = C::RPD * C::DPW * wave + lane / C::CPR, pos = lane % C::CPR;
+    kdma = (uint32_t)(row * C::RB + 16 * (pos ^ k_swz<D, BLK>(row)));
+    vdma = (uint32_t)(row * C::RB + 16 * (pos ^ v_swz<D, BLK>(row)));
   }
   const uint16_t* const kbase = a.k + bh * a.lk * D;
   const uint16_t* const vbase = a.v + bh * a.lk * D;
@@ -330,8 +336,11 @@ void attn_fwd_kernel(AttnArgs a) {
   auto tile_bytes = [&](int kt) -> uint32_t {
     return (kt < 0 || kt >= n_kt) ? 0u : (kt == n_kt - 1 ? last_bytes : (uint32_t)C::TILE_BYTES);
   };
-  auto dma = [&](const uint16_t* base, int blk, uint16_t* slot, const uint32_t* off) {
+  auto dma = [&](const uint16_t* base, int blk, uint16_t* slot, uint32_t off0, uint32_t step) {
     const i32x4 rs = raw_rsrc(base + (int64_t)(blk < 0 ? 0 : blk) * C::TILE, tile_bytes(blk));
+    uint32_t off[C::DPW];
+#pragma unroll
+    for (int i = 0; i < C::DPW; ++i) off[i] = off0 ^ (step * i);
     dma_tile<C::DPW>(lds_addr(slot) + (uint32_t)(C::DPW * wave) * 1024u, off, rs);
   };
 
@@ -440,20 +449,20 @@ void attn_fwd_kernel(AttnArgs a) {
     b2 = fetch(2);
     b3 = fetch(3);
     b4 = fetch(4);
-    dma(kbase, b0, ks0, kdma);
-    dma(kbase, b1, ks1, kdma);
-    dma(kbase, b2, ks2, kdma);
-    dma(vbase, b0, vs0, vdma);
+    dma(kbase, b0, ks0, kdma, 64u);
+    dma(kbase, b1, ks1, kdma, 64u);
+    dma(kbase, b2, ks2, kdma, 64u);
+    dma(vbase, b0, vs0, vdma, 0u);
     wait_vmcnt<3 * C::DPW>();  // K(0)
     __syncthreads();
     scores(ks0, acc_s);
     if (needs_mask(b0)) mask_tile(acc_s, b0);
     apply_max(tile_max(acc_s));
     __syncthreads();  // K slot 0 is free
-    dma(kbase, b3, ks0, kdma);
+    dma(kbase, b3, ks0, kdma, 64u);
     wait_vmcnt<3 * C::DPW>();  // K(1)
     __syncthreads();
-    dma(vbase, b1, vs1, vdma);
+    dma(vbase, b1, vs1, vdma, 0u);
 
     // One step (T = t mod 6 fixes the slots), in two phases:
     //   A: the scores of tile t+1 on the matrix cores while the exponentials of
@@ -474,19 +483,17 @@ void attn_fwd_kernel(AttnArgs a) {
       // ---- phase A
       f32x16 acc_n[C::KT];
       const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
-      uint4 kf[C::KT][C::DS];
-#pragma unroll
-      for (int kt = 0; kt < C::KT; ++kt)
-#pragma unroll
-        for (int s = 0; s < C::DS; ++s) kf[kt][s] = lds_u4(kr, koff[s] + kt * 32 * C::RB);
       uint32_t pk[C::KT][8];  // bf16 pairs of P^T, per 32-key sub-tile
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt) {
+        uint4 kf[C::DS];
+#pragma unroll
+        for (int s = 0; s < C::DS; ++s) kf[s] = lds_u4(kr, koff[s] + kt * 32 * C::RB);
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc_n[kt][e] = 0.f;
 #pragma unroll
         for (int s = 0; s < C::DS; ++s)
-          acc_n[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[kt][s]), qf[s],
+          acc_n[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[s]), qf[s],
                                                               acc_n[kt], 0, 0, 0);
 #pragma unroll
         for (int e = 0; e < 16; e += 2) {
@@ -512,7 +519,7 @@ void attn_fwd_kernel(AttnArgs a) {
       __builtin_amdgcn_sched_barrier(0);  // the phase ends here
       wait_vmcnt<2 * C::DPW>();  // V(t)
       __syncthreads();
-      dma(kbase, b4, kr, kdma);
+      dma(kbase, b4, kr, kdma, 64u);
 
       // ---- phase B: O^T += V^T P^T over 16-key k-steps
 #pragma unroll
@@ -572,7 +579,7 @@ void attn_fwd_kernel(AttnArgs a) {
       __builtin_amdgcn_sched_barrier(0);
       wait_vmcnt<3 * C::DPW>();  // K(t+2)
       __syncthreads();
-      dma(vbase, b2, vr, vdma);
+      dma(vbase, b2, vr, vdma, 0u);
 
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt) acc_s[kt] = acc_n[kt];
@@ -600,30 +607,42 @@ void attn_fwd_kernel(AttnArgs a) {
   }
   __syncthreads();
 
-  // ---- merge the two key halves of each query slice, then write O and lse.
-  // Key half 1 of slice qs leaves its 16 DT accumulators per lane in tile slot
-  // qs (K slots 0-2, then V slot 0) and (m, l) in V slot 1.
+  // ---- with two key parts per tile, merge the parts of each query slice
+  // (part 1 of slice qs leaves its 16 DT accumulators per lane in tile slot qs
+  // -- K slots 0-2, then V slot 0 -- and (m, l) in V slot 1); then write O and
+  // lse.
   l_run = half_swap_sum(l_run);  // both lane halves now hold the slice's partial sum
   constexpr int OB = 16 * C::DT * 64 * 4;  // bytes of one slice's accumulators
   static_assert(OB == C::TILE_BYTES && C::NQS <= 4, "one slice's accumulators per tile slot");
   float* my_o = reinterpret_cast<float*>(qs == 0 ? ks0 : qs == 1 ? ks1 : qs == 2 ? ks2 : vs0);
   float* my_ml = reinterpret_cast<float*>(vs1) + qs * 2 * 64;
-  if (kh == 1) {
-    my_ml[0 * 64 + lane] = m_run;
-    my_ml[1 * 64 + lane] = l_run;
+  if constexpr (C::KSP == 2) {
+    if (kh == 1) {
+      my_ml[0 * 64 + lane] = m_run;
+      my_ml[1 * 64 + lane] = l_run;
 #pragma unroll
-    for (int t = 0; t < C::DT; ++t)
+      for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) my_o[(16 * t + e) * 64 + lane] = acc_o[t][e];
+        for (int e = 0; e < 16; ++e) my_o[(16 * t + e) * 64 + lane] = acc_o[t][e];
+    }
+    __syncthreads();
   }
-  __syncthreads();
   if (kh == 0) {
-    const float m1 = my_ml[0 * 64 + lane], l1 = my_ml[1 * 64 + lane];
+    float m1 = -INFINITY, l1 = 0.f;
+    if constexpr (C::KSP == 2) {
+      m1 = my_ml[0 * 64 + lane];
+      l1 = my_ml[1 * 64 + lane];
+    }
     const float mm = fmaxf(m_run, m1);
     const float a0 = m_run == -INFINITY ? 0.f : exp2f(m_run - mm);
     const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - mm);
     const float l = l_run * a0 + l1 * a1;
     const float inv = l > 0.f ? 1.f / l : 0.f;
+    // the other key part's weighted accumulator (none with one part per tile)
+    auto other = [&](int t, int e) -> float {
+      if constexpr (C::KSP == 2) return my_o[(16 * t + e) * 64 + lane] * a1;
+      else return 0.f;
+    };
     if (SPLIT && q_ok) {
       const int64_t prow = (work * kSplits + split) * BLK + qs * 32 + l32;
       _Float16* po = reinterpret_cast<_Float16*>(a.part_o) + prow * D;
@@ -635,7 +654,7 @@ void attn_fwd_kernel(AttnArgs a) {
           f16x4 w;
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            w[e] = (_Float16)((acc_o[t][4 * g + e] * a0 + my_o[(16 * t + 4 * g + e) * 64 + lane] * a1) * inv);
+            w[e] = (_Float16)((acc_o[t][4 * g + e] * a0 + other(t, 4 * g + e)) * inv);
           *reinterpret_cast<f16x4*>(po + d) = w;
         }
       if (hh == 0) {
@@ -653,7 +672,7 @@ void attn_fwd_kernel(AttnArgs a) {
           float o[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            o[e] = (acc_o[t][4 * g + e] * a0 + my_o[(16 * t + 4 * g + e) * 64 + lane] * a1) * inv;
+            o[e] = (acc_o[t][4 * g + e] * a0 + other(t, 4 * g + e)) * inv;
           uint2 w;
           w.x = pack2_bf16(o[0], o[1]);
           w.y = pack2_bf16(o[2], o[3]);
