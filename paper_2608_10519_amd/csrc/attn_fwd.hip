@@ -2,21 +2,20 @@
 //
 // Work decomposition.  One work-group per (batch*head, query block of BLK
 // rows, key range), launched so that the eight XCDs stream disjoint key ranges
-// of the same head (see the work-item decode below).  Keys are processed in
-// tiles of 64 (a key block of BLK keys is BLK/64 tiles), so a 128-row query
-// block shares each K and V tile among four query slices.  The work-group has
-// 2 * BLK/32 wavefronts: wave w owns the 32-row query slice (w % (BLK/32)) and
-// the 32-key half (w / (BLK/32)) of every tile, so each wave touches only half
-// of each K and V tile and two waves per SIMD stay resident (<= 256 VGPRs
-// each).
+// of the same head (see the work-item decode below).  The work-group has one
+// wavefront per 32-row query slice (two for 64-row blocks, four for 128-row
+// blocks), and every wave takes the whole of each key tile, so no key is ever
+// split between waves.  Keys come in tiles of KB = BLK / 2 (32 keys for 64-row
+// blocks, 64 for 128-row blocks; a key block is two tiles), which sizes the LDS
+// ring at 40 KB (80 KB) per work-group at D = 128: four (two) work-groups per
+// CU, two waves per SIMD, each under 256 VGPRs.
 //
-// Per key block of the query block's ascending list:
-//   * K and V tiles (64 x D each) go from global memory straight into LDS
+// Per tile of the query block's ascending key-block list:
+//   * K and V tiles (KB x D) go from global memory straight into LDS
 //     (buffer_load ... lds, 1 KB per wave instruction, coalesced), with no
-//     VGPR staging.  LDS holds a ring of three K tiles and two V tiles: the K
-//     tile is needed one step before the V tile of the same block, and the
-//     loads of K(t+3) and V(t+1) are issued at the start of step t, so one
-//     barrier per step suffices;
+//     VGPR staging.  LDS holds a ring of three K tiles and two V tiles; each
+//     step has two barrier phases (scores, then P V), and each phase's barrier
+//     frees the slot the next loads go into;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (fp32 accumulate).  The
 //     transpose leaves each lane holding 16 keys of ONE query column -- exactly
 //     the B-operand layout P^T needs -- so the softmax state is lane-local up to
@@ -30,8 +29,7 @@
 //     transpose read ds_read_b64_tr_b16 (in each 16-lane group, source lane s
 //     points at V[r0 + s/4][4 (c0 + s%4)], and lane j receives
 //     V[r0 .. r0+3][4 c0 + j]: 4 keys of one d column).
-// The two key halves of a query slice each hold a partial (m, l, O); they are
-// merged once through LDS at the end.  O = O^T / l in bf16, lse = ln2*(m + log2 l).
+// O = O^T / l in bf16, lse = ln2*(m + log2 l).
 //
 // MFMA layouts (v_mfma_f32_32x32x16_bf16, lane l, h = l / 32):
 //   A[m][k]: m = l % 32, k = 8h + i (i = 0..7 of the lane's bf16x8)
@@ -55,17 +53,12 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 template <int D, int BLK>
 struct AttnCfg {
-  static constexpr int KB = 64;               // keys per K/V tile
+  static constexpr int KB = BLK / 2;          // keys per K/V tile
   static constexpr int SUB = BLK / KB;        // tiles per key block (list entry)
   static constexpr int NQS = BLK / 32;        // 32-row query slices
-  // key parts per tile: with 64-row blocks two waves share a slice, each
-  // taking one 32-key half of every tile; with 128-row blocks one wave takes
-  // the whole tile, so the four waves of a work-group never split a key
-  static constexpr int KSP = BLK == 128 ? 1 : 2;
-  static constexpr int NW = KSP * NQS;        // waves: (query slice, key part of a tile)
+  static constexpr int NW = NQS;              // waves: one per query slice
   static constexpr int NT = 64 * NW;          // threads
-  static constexpr int KH = KB / KSP;         // keys per key part
-  static constexpr int KT = KH / 32;          // 32-key sub-tiles per wave and step
+  static constexpr int KT = KB / 32;          // 32-key sub-tiles per step
   static constexpr int DS = D / 16;           // MFMA k-steps over D
   static constexpr int DT = D / 32;           // 32-row d tiles of O^T
   static constexpr int RB = D * 2;            // bytes per K/V row
@@ -76,7 +69,7 @@ struct AttnCfg {
   static constexpr int RPD = 1024 / RB;       // rows per direct-to-LDS wave load (64 lanes x 16 B)
   static constexpr int DPW = TILE_BYTES / 1024 / NW;  // direct loads per wave and tile
   static_assert(DPW * NW * 1024 == TILE_BYTES, "tile split over the waves");
-  static_assert(KT * 32 * KSP == KB, "key parts");
+  static_assert(KT * 32 == KB, "32-key sub-tiles");
   static_assert(SUB * KB == BLK, "whole tiles per key block");
 };
 
@@ -191,7 +184,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 template <int D, int BLK, bool DENSE, bool SPLIT>
-__global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_kernel(AttnArgs a) {
   using C = AttnCfg<D, BLK>;
   // Ring of three K tiles and two V tiles.  Step t reads K of tile t+1 (the
@@ -223,8 +216,7 @@ void attn_fwd_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const int l32 = lane % 32, hh = lane / 32;
-  const int qs = wave % C::NQS;   // query slice
-  const int kh = wave / C::NQS;   // key half
+  const int qs = wave;  // query slice
 
   // ---- Q fragment (B operand of S^T = K Q^T): Q[q][16 s + 8 hh .. +7]
   const int64_t q_row = (int64_t)qb * BLK + qs * 32 + l32;
@@ -345,22 +337,22 @@ void attn_fwd_kernel(AttnArgs a) {
   };
 
   // ---- per-lane LDS read offsets (bytes within a tile)
-  // K operand of S^T: row kh KH + 32 kt + l32, logical chunk 2 s + hh
+  // K operand of S^T: row 32 kt + l32, logical chunk 2 s + hh
   uint32_t koff[C::DS];
   {
-    const int r = kh * C::KH + l32;
+    const int r = l32;
 #pragma unroll
     for (int s = 0; s < C::DS; ++s) koff[s] = (uint32_t)(r * C::RB + 16 * ((2 * s + hh) ^ k_swz<D, BLK>(r)));
   }
   // V^T operand through the transpose read: in each 16-lane group g, source lane
-  // sl points at row R = kh KH + 4 hh + sl / 4 (+ 32 kt + 16 half + 8 for the
+  // sl points at row R = 4 hh + sl / 4 (+ 32 kt + 16 half + 8 for the
   // second read), bytes 64 t + 32 (g % 2) + 8 (sl % 4), i.e. logical chunk
   // 4 t + 2 (g % 2) + (sl % 4) / 2, half (sl % 2); lane j then receives
   // V[R0 .. R0+3][4 c0 + j], four keys of one d column
   uint32_t voff[C::DT];
   {
     const int grp = lane >> 4, sl = lane & 15;
-    const int r = kh * C::KH + 4 * hh + (sl >> 2);
+    const int r = 4 * hh + (sl >> 2);
 #pragma unroll
     for (int t = 0; t < C::DT; ++t) {
       const int c = 4 * t + 2 * (grp & 1) + ((sl & 3) >> 1);
@@ -393,7 +385,7 @@ void attn_fwd_kernel(AttnArgs a) {
       for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int key = kh * C::KH + kt * 32 + 8 * (e / 4) + 4 * hh + (e % 4);
+          const int key = kt * 32 + 8 * (e / 4) + 4 * hh + (e % 4);
           if (blk < 0 || key0 + key >= a.lk) acc[kt][e] = -INFINITY;
         }
     }
@@ -528,7 +520,7 @@ void attn_fwd_kernel(AttnArgs a) {
         for (int half = 0; half < 2; ++half) {
           // accumulators a = 8 half + i of sub-tile kt hold keys
           //   base + 4 hh + i (i = 0..3) and base + 8 + 4 hh + (i - 4) (i = 4..7),
-          // base = kh * KH + 32 kt + 16 half; the two transpose reads fetch the
+          // base = 32 kt + 16 half; the two transpose reads fetch the
           // same keys of V for d = 32 t + l % 32.
           uint4 pu;
           pu.x = pk[kt][4 * half + 0];
@@ -605,44 +597,13 @@ void attn_fwd_kernel(AttnArgs a) {
     }
     wait_vmcnt<0>();  // loads past the end of the list still write LDS
   }
-  __syncthreads();
 
-  // ---- with two key parts per tile, merge the parts of each query slice
-  // (part 1 of slice qs leaves its 16 DT accumulators per lane in tile slot qs
-  // -- K slots 0-2, then V slot 0 -- and (m, l) in V slot 1); then write O and
-  // lse.
-  l_run = half_swap_sum(l_run);  // both lane halves now hold the slice's partial sum
-  constexpr int OB = 16 * C::DT * 64 * 4;  // bytes of one slice's accumulators
-  static_assert(OB == C::TILE_BYTES && C::NQS <= 4, "one slice's accumulators per tile slot");
-  float* my_o = reinterpret_cast<float*>(qs == 0 ? ks0 : qs == 1 ? ks1 : qs == 2 ? ks2 : vs0);
-  float* my_ml = reinterpret_cast<float*>(vs1) + qs * 2 * 64;
-  if constexpr (C::KSP == 2) {
-    if (kh == 1) {
-      my_ml[0 * 64 + lane] = m_run;
-      my_ml[1 * 64 + lane] = l_run;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) my_o[(16 * t + e) * 64 + lane] = acc_o[t][e];
-    }
-    __syncthreads();
-  }
-  if (kh == 0) {
-    float m1 = -INFINITY, l1 = 0.f;
-    if constexpr (C::KSP == 2) {
-      m1 = my_ml[0 * 64 + lane];
-      l1 = my_ml[1 * 64 + lane];
-    }
-    const float mm = fmaxf(m_run, m1);
-    const float a0 = m_run == -INFINITY ? 0.f : exp2f(m_run - mm);
-    const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - mm);
-    const float l = l_run * a0 + l1 * a1;
+  // ---- write O and lse
+  l_run = half_swap_sum(l_run);  // both lane halves now hold the query's row sum
+  {
+    const float mm = m_run;
+    const float l = l_run;
     const float inv = l > 0.f ? 1.f / l : 0.f;
-    // the other key part's weighted accumulator (none with one part per tile)
-    auto other = [&](int t, int e) -> float {
-      if constexpr (C::KSP == 2) return my_o[(16 * t + e) * 64 + lane] * a1;
-      else return 0.f;
-    };
     if (SPLIT && q_ok) {
       const int64_t prow = (work * kSplits + split) * BLK + qs * 32 + l32;
       _Float16* po = reinterpret_cast<_Float16*>(a.part_o) + prow * D;
@@ -654,7 +615,7 @@ void attn_fwd_kernel(AttnArgs a) {
           f16x4 w;
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            w[e] = (_Float16)((acc_o[t][4 * g + e] * a0 + other(t, 4 * g + e)) * inv);
+            w[e] = (_Float16)(acc_o[t][4 * g + e] * inv);
           *reinterpret_cast<f16x4*>(po + d) = w;
         }
       if (hh == 0) {
@@ -672,7 +633,7 @@ void attn_fwd_kernel(AttnArgs a) {
           float o[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            o[e] = (acc_o[t][4 * g + e] * a0 + other(t, 4 * g + e)) * inv;
+            o[e] = acc_o[t][4 * g + e] * inv;
           uint2 w;
           w.x = pack2_bf16(o[0], o[1]);
           w.y = pack2_bf16(o[2], o[3]);
