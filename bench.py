@@ -374,6 +374,22 @@ def main() -> int:
         log(f"selector from cold caches: median {np.median(cold):.3f} ms "
             f"({read_bytes / (np.median(cold) * 1e-3) / 1e12:.2f} TB/s of Q+K over the whole selector call)")
 
+    n_k = -(-Lk // w.block)
+    if n_k <= S.FUSED_MAX_BLOCKS:
+        # the selector with scores and selection fused in one kernel (S kept in
+        # LDS), on lists of its own
+        fnum, fidx = torch.empty_like(r.num), torch.empty_like(r.idx)
+
+        def fused():
+            S.sparstar_score_blocks(r.q, r.k, w.block, r.budget, r.keep, kv_stride=r.stride, workspace=r.ws,
+                                    out=(fnum, fidx), fused=True)
+
+        f_ms = r.timed(fused, reps=10, warm=2)
+        out["breakdown_ms"]["score_blocks_fused"] = float(np.mean(f_ms))
+        out["breakdown_ms"]["score_blocks_fused_median"] = float(np.median(f_ms))
+        log(f"fused score/select selector: {np.mean(f_ms):.3f} ms (separate kernels {np.mean(sel_ms):.3f} ms)")
+        del fnum, fidx
+
     if not args.no_graph:
         # the same step captured once in a HIP graph (both calls only launch
         # kernels on the stream) and replayed K times

@@ -117,6 +117,27 @@ int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq
                           int n_keep, int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride, float* scores,
                           void* workspace, size_t workspace_bytes, void* stream);
 
+/* Most key blocks per row that sparstar_score_blocks_fused accepts. */
+#define SPARSTAR_FUSED_MAX_BLOCKS 2304
+
+/*
+ * The selector of sparstar_score_blocks with the scores and the selection in
+ * one kernel: S of 16 query blocks of one head is computed into LDS and each
+ * row is selected from there, so S never reaches memory (the fusion that
+ * Section 5.3's mask construction suggests).  Same arguments, results and
+ * errors as sparstar_score_blocks with scores == NULL, except that rows of more
+ * than SPARSTAR_FUSED_MAX_BLOCKS key blocks return SPARSTAR_ERR_UNSUPPORTED.
+ * The scores are summed in another order than the separate score kernel's, so
+ * a row whose k-th and (k+1)-th scores are within fp32 rounding may select
+ * differently.  At the 720p shape (2258 key blocks) the separate kernels are
+ * faster: one such work-group fills a CU's LDS, so its score and selection
+ * phases cannot overlap those of another.
+ */
+int sparstar_score_blocks_fused(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
+                                int block_size, const double* budget, int n_budget, const sparstar_range* keep,
+                                int n_keep, int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
 /*
  * Bytes of device workspace that lets the attention calls below split the key
  * blocks of every query block into 16 contiguous ranges (two per XCD of the

@@ -25,7 +25,10 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 __device__ __forceinline__ bool keep_block(const KeepBlocks& kb, int j) {
   bool r = false;
 #pragma unroll
-  for (int t = 0; t < kMaxKeep; ++t) r |= (t < kb.n) & (j >= kb.begin[t]) & (j < kb.end[t]);
+  for (int t = 0; t < kMaxKeep; ++t) {
+    if (t >= kb.n) break;  // uniform: a kernel argument
+    r |= (j >= kb.begin[t]) & (j < kb.end[t]);
+  }
   return r;
 }
 

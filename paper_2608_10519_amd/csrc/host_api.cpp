@@ -201,10 +201,10 @@ extern "C" size_t sparstar_score_workspace_bytes(int B, int H, int64_t Lq, int64
   return ws_layout(B, H, Lq, Lk, D, block_size).total;
 }
 
-extern "C" int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
-                                     int block_size, const double* budget, int n_budget, const sparstar_range* keep,
-                                     int n_keep, int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride,
-                                     float* scores, void* workspace, size_t workspace_bytes, void* stream) {
+static int score_common(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D, int block_size,
+                        const double* budget, int n_budget, const sparstar_range* keep, int n_keep,
+                        int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride, float* scores, void* workspace,
+                        size_t workspace_bytes, void* stream, bool fused) {
   using namespace sparstar;
   if (int rc = check_sizes(B, H, Lq, Lk, D, block_size)) return rc;
   // With Lq == 0 there is nothing to read or write on the query side.
@@ -230,6 +230,9 @@ extern "C" int sparstar_score_blocks(const void* q, const void* k, int B, int H,
     return fail(SPARSTAR_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, wl.total);
   if (scores && (reinterpret_cast<uintptr_t>(scores) & 3u) != 0)
     return fail(SPARSTAR_ERR_INVALID_ARG, "scores must be 4-byte aligned");
+  if (fused && nk > kFusedMaxBlocks)
+    return fail(SPARSTAR_ERR_UNSUPPORTED, "fused scores and selection take at most %d key blocks (got %lld)",
+                kFusedMaxBlocks, (long long)nk);
   if (nq == 0) return ok();
 
   const int bh = B * H;
@@ -243,8 +246,16 @@ extern "C" int sparstar_score_blocks(const void* q, const void* k, int B, int H,
               int(nk), kb};
   hipError_t e = launch_pool(pa, D, block_size, st);
   if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "pool launch: %s", hipGetErrorString(e));
+  const float tau = float(1.0 / sqrt(double(D)));
+  if (fused) {
+    // scores and selection in one kernel, S kept in LDS
+    ScoreSelectArgs fa{q_bar, k_bar, kv_num_blocks, kv_indices, bh, int(nq), int(nk), H, kv_stride, D, tau, kb, hb};
+    e = launch_score_select(fa, st);
+    if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "score/select launch: %s", hipGetErrorString(e));
+    return ok();
+  }
   if (n_sel > 0) {
-    ScoreArgs sa{q_bar, k_bar, s, bh, int(nq), int(nk), float(1.0 / sqrt(double(D))), kb};
+    ScoreArgs sa{q_bar, k_bar, s, bh, int(nq), int(nk), tau, kb};
     e = launch_score(sa, D, st);
     if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "score launch: %s", hipGetErrorString(e));
   }
@@ -252,6 +263,23 @@ extern "C" int sparstar_score_blocks(const void* q, const void* k, int B, int H,
   e = launch_select(sel, st);
   if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "select launch: %s", hipGetErrorString(e));
   return ok();
+}
+
+extern "C" int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
+                                     int block_size, const double* budget, int n_budget, const sparstar_range* keep,
+                                     int n_keep, int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride,
+                                     float* scores, void* workspace, size_t workspace_bytes, void* stream) {
+  return score_common(q, k, B, H, Lq, Lk, D, block_size, budget, n_budget, keep, n_keep, kv_num_blocks, kv_indices,
+                      kv_stride, scores, workspace, workspace_bytes, stream, false);
+}
+
+extern "C" int sparstar_score_blocks_fused(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
+                                           int block_size, const double* budget, int n_budget,
+                                           const sparstar_range* keep, int n_keep, int32_t* kv_num_blocks,
+                                           int32_t* kv_indices, int kv_stride, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  return score_common(q, k, B, H, Lq, Lk, D, block_size, budget, n_budget, keep, n_keep, kv_num_blocks, kv_indices,
+                      kv_stride, nullptr, workspace, workspace_bytes, stream, true);
 }
 
 extern "C" size_t sparstar_attn_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
@@ -344,6 +372,7 @@ extern "C" int sparstar_retained_mass(const float* lse_sel, const float* lse_all
 }
 
 static_assert(sparstar::kTopkMaxRows == SPARSTAR_MAX_MASS_ROWS, "sampled-row limit");
+static_assert(sparstar::kFusedMaxBlocks == SPARSTAR_FUSED_MAX_BLOCKS, "fused row limit");
 
 static int check_topk_sizes(int B, int H, int64_t Lk, int n_rows) {
   if (B < 1 || H < 1 || int64_t(B) * H > 65535)

@@ -51,6 +51,23 @@ struct SelectArgs {
   HeadBudgets budget;
 };
 
+// Scores and selection in one kernel (S kept in LDS): kFusedRows query blocks
+// of one head per work-group, one wave per row for the selection.  Rows of up
+// to kFusedMaxBlocks key blocks (16 rows x 2304 x 4 B = 144 KB of LDS).
+constexpr int kFusedRows = 16;
+constexpr int kFusedMaxBlocks = 2304;
+
+struct ScoreSelectArgs {
+  const float* q_bar;      // [BH, n_q, D]
+  const float* k_bar;      // [BH, n_k, D]
+  int32_t* kv_num_blocks;  // [BH, n_q]
+  int32_t* kv_indices;     // [BH, n_q, stride]
+  int bh, n_q, n_k, heads, stride, d;
+  float tau;               // D^-1/2
+  KeepBlocks keep;
+  HeadBudgets budget;
+};
+
 struct AttnArgs {
   const uint16_t* q;  // [BH, Lq, D]
   const uint16_t* k;  // [BH, Lk, D]
@@ -97,6 +114,7 @@ struct TopkArgs {
 hipError_t launch_pool(const PoolArgs& a, int d, int block, hipStream_t stream);
 hipError_t launch_score(const ScoreArgs& a, int d, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+hipError_t launch_score_select(const ScoreSelectArgs& a, hipStream_t stream);
 hipError_t launch_attn(const AttnArgs& a, int d, int block, bool dense, hipStream_t stream);
 hipError_t launch_retained_mass(const float* lse_sel, const float* lse_all, int64_t n, float* mass,
                                 hipStream_t stream);

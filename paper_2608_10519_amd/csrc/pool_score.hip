@@ -4,7 +4,7 @@
 //        is zero-padded and still divided by the nominal b.  One work-group per
 //        block streams its b x D bf16 tile once with 16-byte loads (HBM-bound;
 //        algorithmic bytes = 2*D per token read + 4*D per block written).
-// score: S_ij = tau * qbar_i . kbar_j in fp32 FMA for selectable j; forced key
+// score: S_ij = tau * qbar_i . kbar_j in fp32 (MFMA) for selectable j; forced key
 //        blocks are neither pooled nor scored (Section 5.2), their S columns are
 //        left untouched.
 #include "device_common.h"
@@ -69,16 +69,26 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// score: one work-group per (bh, 64 query blocks, 64 key blocks) tile,
-// 256 threads, each a 4x4 sub-tile; D streamed through LDS in chunks of 32.
+// score: one work-group per (bh, 64 query blocks, 64 key blocks) tile of S,
+// four waves, each a 32 x 32 sub-tile on v_mfma_f32_32x32x2_f32 (fp32
+// products, fp32 accumulation).  D is streamed through LDS in chunks of SKC
+// columns (coalesced 16-byte loads), which keeps a work-group at 18 KB of LDS
+// so that many share a CU; rows are padded by 4 floats, which makes the
+// per-lane row reads below free of bank conflicts.
+//
+// MFMA operands (lane l, h = l / 32): A[m][k] = qbar[m = l % 32][d],
+// B[k][n] = kbar[n = l % 32][d] with k = h; within a chunk MFMA s reads
+// d = (SKC/2) h + s, so each lane walks its own half-row with 16-byte reads.
+// C[m][n] sits at accumulator a with n = l % 32, m = 8 (a / 4) + 4 h + (a % 4).
 // ---------------------------------------------------------------------------
 constexpr int ST = 64;   // tile edge (query blocks and key blocks)
 constexpr int SKC = 32;  // D chunk
 
 template <int D>
 __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
-  __shared__ float qs[SKC][ST + 4];
-  __shared__ float ks[SKC][ST + 4];
+  constexpr int RS = SKC + 4;  // padded LDS row (floats)
+  __shared__ __attribute__((aligned(16))) float qs[ST * RS];
+  __shared__ __attribute__((aligned(16))) float ks[ST * RS];
   const int tiles_i = (a.n_q + ST - 1) / ST;
   const int tiles_j = (a.n_k + ST - 1) / ST;
   int64_t wg = blockIdx.x;
@@ -90,51 +100,49 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
 
   const float* qb = a.q_bar + bh * (int64_t)a.n_q * D;
   const float* kb = a.k_bar + bh * (int64_t)a.n_k * D;
-  const int t = threadIdx.x, tx = t % 16, ty = t / 16;
-
-  float acc[4][4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) acc[r][c] = 0.f;
-
-  // loader: 64 rows x 32 floats = 512 float4; thread t loads rows lr and lr + 32
+  const int t = threadIdx.x;
+  const int wave = t / 64, lane = t % 64, l32 = lane % 32, h = lane / 32;
+  const int wq = wave / 2, wk = wave % 2;  // the wave's 32 x 32 sub-tile
+  // loader: 64 rows x SKC floats = 512 float4 per tile; thread t loads rows lr and lr + 32
   const int lr = t / 8, lc = (t % 8) * 4;
+  const bool q_ok[2] = {i0 + lr < a.n_q, i0 + lr + 32 < a.n_q};
+  const bool k_ok[2] = {j0 + lr < a.n_k, j0 + lr + 32 < a.n_k};
+
+  f32x16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
   for (int d0 = 0; d0 < D; d0 += SKC) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int row = lr + 32 * h;
+    for (int u = 0; u < 2; ++u) {
+      const int row = lr + 32 * u;
       float4 qv = make_float4(0.f, 0.f, 0.f, 0.f), kv = qv;
-      if (i0 + row < a.n_q) qv = *reinterpret_cast<const float4*>(qb + (int64_t)(i0 + row) * D + d0 + lc);
-      if (j0 + row < a.n_k) kv = *reinterpret_cast<const float4*>(kb + (int64_t)(j0 + row) * D + d0 + lc);
-      qs[lc + 0][row] = qv.x; qs[lc + 1][row] = qv.y; qs[lc + 2][row] = qv.z; qs[lc + 3][row] = qv.w;
-      ks[lc + 0][row] = kv.x; ks[lc + 1][row] = kv.y; ks[lc + 2][row] = kv.z; ks[lc + 3][row] = kv.w;
+      if (q_ok[u]) qv = *reinterpret_cast<const float4*>(qb + (int64_t)(i0 + row) * D + d0 + lc);
+      if (k_ok[u]) kv = *reinterpret_cast<const float4*>(kb + (int64_t)(j0 + row) * D + d0 + lc);
+      *reinterpret_cast<float4*>(qs + row * RS + lc) = qv;
+      *reinterpret_cast<float4*>(ks + row * RS + lc) = kv;
     }
     __syncthreads();
-#pragma unroll 8
-    for (int d = 0; d < SKC; ++d) {
-      const float4 qv = *reinterpret_cast<const float4*>(&qs[d][ty * 4]);
-      const float4 kv = *reinterpret_cast<const float4*>(&ks[d][tx * 4]);
-      const float qa[4] = {qv.x, qv.y, qv.z, qv.w};
-      const float ka[4] = {kv.x, kv.y, kv.z, kv.w};
+    const float* qa = qs + (wq * 32 + l32) * RS + (SKC / 2) * h;
+    const float* kc = ks + (wk * 32 + l32) * RS + (SKC / 2) * h;
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) acc[r][c] = fmaf(qa[r], ka[c], acc[r][c]);
+    for (int i = 0; i < SKC / 8; ++i) {
+      const float4 x = *reinterpret_cast<const float4*>(qa + 4 * i);
+      const float4 y = *reinterpret_cast<const float4*>(kc + 4 * i);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.x, y.x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.y, y.y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.z, y.z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.w, y.w, acc, 0, 0, 0);
     }
     __syncthreads();
   }
 
-  float* srow = a.s + bh * (int64_t)a.n_q * a.n_k;
+  const int j = j0 + wk * 32 + l32;
+  if (j >= a.n_k || keep_block(a.keep, j)) return;  // no barrier below
+  float* scol = a.s + bh * (int64_t)a.n_q * a.n_k + j;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int j = j0 + tx * 4 + c;
-    if (j >= a.n_k || keep_block(a.keep, j)) continue;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int i = i0 + ty * 4 + r;
-      if (i < a.n_q) srow[(int64_t)i * a.n_k + j] = a.tau * acc[r][c];
-    }
+  for (int e = 0; e < 16; ++e) {
+    const int i = i0 + wq * 32 + 8 * (e / 4) + 4 * h + (e % 4);
+    if (i < a.n_q) scol[(int64_t)i * a.n_k] = a.tau * acc[e];
   }
 }
 

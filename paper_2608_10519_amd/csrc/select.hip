@@ -2,17 +2,24 @@
 // written as the forward-only block mask of Section 5.3: kv_num_blocks and the
 // ascending kv_indices row.
 //
-// One wavefront per score row.  The k-th largest selectable score is found
-// exactly by a 4-pass radix select (8 bits per pass) on order-preserving 32-bit
-// keys, with the digit histogram in LDS.  Equal scores are broken toward the
-// lower block index.  A final pass walks the row in ascending block order and
-// compacts {forced} U {selected} with wave ballots, so the list comes out
-// sorted without a sort.
+// One wavefront per score row, on order-preserving 32-bit keys of the fp32
+// scores.  Equal scores are broken toward the lower block index.  A final pass
+// walks the row in ascending block order and compacts {forced} U {selected}
+// with wave ballots, so the list comes out sorted without a sort.
+//
+// Rows of up to kSelRegMaxBlocks blocks keep their keys in registers (key c of
+// lane L is block 64 c + L) and find the k-th largest key bit by bit from the
+// top: a candidate threshold t is kept when at least k keys are >= t, counted
+// with one compare and one ballot popcount per 64 keys, with no atomics.  The
+// search stops early once exactly k keys are >= t.  Longer rows stream from
+// memory through a 4-pass radix select (8 bits per pass) with the digit
+// histogram in LDS.
 #include "device_common.h"
 
 namespace sparstar {
 
 constexpr int kSelWaves = 4;
+constexpr int kSelRegMaxBlocks = 3584;  // 56 keys per lane
 
 // fp32 -> unsigned key with the same order (-0 is folded onto +0).
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -106,150 +113,225 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_kernel(SelectArgs a) {
   if (lane == 0) a.kv_num_blocks[r] = pos;
 }
 
-// Rows of up to kSelCachedMaxBlocks blocks: each wave reads its row once,
-// keeps the order keys in LDS (forced blocks as 0, corrected for in the
-// counts) and walks it four keys per lane per LDS read in all five passes.
-constexpr int kSelCachedMaxBlocks = 3584;  // 4 waves x 3584 x 4 B = 56 KB (+ 4 KB of histograms)
-
-// sum of v over the lanes below this one, for 0 <= v <= 7
-__device__ __forceinline__ uint32_t lanes_below_sum(uint32_t v) {
-  uint32_t r = 0;
+// Forced blocks and blocks past n_k hold key 0, below every real key (the
+// smallest order key of a non-NaN float is 0x007fffff), so they never count.
+//
+// Selection of one row whose keys sit in registers: key[c] of lane L is the key
+// of block 64 c + L.  Every lane of the wave calls it.
+template <int C>
+__device__ __forceinline__ void select_row_regs(const uint32_t (&key)[C], int n_k, int kk, const KeepBlocks& keep,
+                                                int lane, int32_t* out, int32_t* num_out) {
+  // thr, take_ties: take every candidate with key > thr and the first
+  // take_ties candidates (in block order) with key == thr
+  uint32_t thr = 0xffffffffu, take_ties = 0;  // kk == 0: nothing selectable
+  if (kk > 0) {
+    uint32_t t = 0;
+    bool exact = false;
+    for (int b = 31; b >= 0; --b) {
+      const uint32_t tt = t | (1u << b);
+      int n = 0;
 #pragma unroll
-  for (int b = 0; b < 3; ++b) r += (uint32_t)lanes_below(__ballot((v >> b) & 1u)) << b;
-  return r;
-}
-
-__global__ __launch_bounds__(64 * kSelWaves) void select_cached_kernel(SelectArgs a) {
-  __shared__ uint32_t hist[kSelWaves][256];
-  extern __shared__ uint4 row_keys[];  // [kSelWaves][quads] order keys, 4 per entry
-  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-  const int64_t row = (int64_t)blockIdx.x * kSelWaves + wave;
-  const bool live = row < a.rows;  // every wave runs the same loop trip counts
-  const int64_t r = live ? row : 0;
-  const int h = (int)((r / a.n_q) % a.heads);
-  const int kk = a.budget.k[h];
-  const float* s = a.s + r * a.n_k;
-  const int quads = (a.n_k + 3) / 4;
-  const int rounds = (quads + 63) / 64;  // 256 keys per round
-  uint4* const keys = row_keys + (size_t)wave * quads;
-
-  // fill: key of block j at keys[j / 4].(j % 4); forced and padding blocks 0
-  uint32_t n_forced = 0;
-  for (int q = lane; q < quads; q += 64) {
-    uint32_t k4[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j = 4 * q + e;
-      const bool forced = j < a.n_k && keep_block(a.keep, j);
-      k4[e] = (j < a.n_k && !forced) ? order_key(s[j]) : 0u;
-      n_forced += forced;
-    }
-    keys[q] = make_uint4(k4[0], k4[1], k4[2], k4[3]);
-  }
-  n_forced = (uint32_t)__reduce_add_sync(~0ull, n_forced);
-
-  uint32_t prefix = 0, mask = 0;
-  uint32_t rem = (uint32_t)kk;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) hist[wave][lane * 4 + e] = 0;
-    __syncthreads();
-    for (int c = 0; c < rounds; ++c) {
-      const int q = c * 64 + lane;
-      if (q < quads) {
-        const uint4 v = keys[q];
-        const uint32_t k4[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if ((k4[e] & mask) == prefix) atomicAdd(&hist[wave][(k4[e] >> shift) & 255u], 1u);
+      for (int c = 0; c < C; ++c) n += __builtin_popcountll(__ballot(key[c] >= tt));
+      if (n >= kk) {
+        t = tt;
+        if (n == kk) {
+          exact = true;
+          break;
+        }
       }
     }
-    __syncthreads();
-    // forced blocks and the padding past n_k were counted as key 0
-    if (lane == 0 && prefix == 0) hist[wave][0] -= n_forced + (uint32_t)(4 * quads - a.n_k);
-    __syncthreads();
-    // The digit d of the rem-th largest key: count(bins > d) < rem <= count(bins >= d).
-    uint32_t cnt[4], own = 0;
+    // t >= 1 here: the kk <= n_sel real keys are all >= 1
+    if (exact) {
+      thr = t - 1;  // the keys >= t are exactly the kk largest
+    } else {
+      // t is the kk-th largest key; the keys above it are all taken
+      int n_gt = 0;
+      if (t != 0xffffffffu) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) { cnt[e] = hist[wave][lane * 4 + e]; own += cnt[e]; }
-    uint32_t suffix = own;  // sum over lanes >= lane
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t o = __shfl_down(suffix, off, 64);
-      if (lane + off < 64) suffix += o;
-    }
-    uint32_t above = suffix - own;  // keys in bins above this lane's four
-    int found = -1;
-    uint32_t new_rem = 0;
-#pragma unroll
-    for (int e = 3; e >= 0; --e) {
-      if (found < 0 && rem > 0 && above < rem && above + cnt[e] >= rem) {
-        found = lane * 4 + e;
-        new_rem = rem - above;
+        for (int c = 0; c < C; ++c) n_gt += __builtin_popcountll(__ballot(key[c] > t));
       }
-      above += cnt[e];
+      thr = t;
+      take_ties = (uint32_t)(kk - n_gt);
     }
-    const uint64_t who = __ballot(found >= 0);
-    if (who != 0) {
-      const int src = __builtin_ctzll(who);
-      const int digit = __shfl(found, src, 64);
-      rem = (uint32_t)__shfl((int)new_rem, src, 64);
-      prefix |= (uint32_t)digit << shift;
-      mask |= 255u << shift;
-    }
-    __syncthreads();
   }
-  // kk == 0 (no selectable block): select nothing.
-  const uint32_t thr = kk > 0 ? prefix : 0xffffffffu;
-  const uint32_t take_ties = kk > 0 ? rem : 0u;
-
-  if (!live) return;
-  // compaction in ascending block order: lane L holds blocks 4 (64 c + L) + e,
-  // so a block's rank is (lanes below) + (earlier e of the same lane)
-  int32_t* out = a.kv_indices + r * a.stride;
   int pos = 0;
   uint32_t ties = 0;
-  for (int c = 0; c < rounds; ++c) {
-    const int q = c * 64 + lane;
-    const uint4 v = q < quads ? keys[q] : make_uint4(0, 0, 0, 0);
-    const uint32_t k4[4] = {v.x, v.y, v.z, v.w};
-    bool forced[4], cand[4], tie[4];
-    uint32_t n_tie = 0;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j = 4 * q + e;
-      const bool valid = j < a.n_k;
-      forced[e] = valid && keep_block(a.keep, j);
-      cand[e] = valid && !forced[e];
-      tie[e] = cand[e] && k4[e] == thr;
-      n_tie += tie[e];
-    }
-    uint32_t tie_rank = ties + lanes_below_sum(n_tie);
-    bool take[4];
-    uint32_t n_take = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      take[e] = forced[e] || (cand[e] && (k4[e] > thr || (tie[e] && tie_rank < take_ties)));
-      tie_rank += tie[e];
-      n_take += take[e];
-    }
-    uint32_t at = (uint32_t)pos + lanes_below_sum(n_take);
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (take[e]) out[at++] = 4 * q + e;
-    pos += (int)__reduce_add_sync(~0ull, n_take);
-    ties += (uint32_t)__reduce_add_sync(~0ull, n_tie);
+  for (int c = 0; c < C; ++c) {
+    if (64 * c >= n_k) break;
+    const int j = 64 * c + lane;
+    const bool valid = j < n_k;
+    const bool forced = valid && keep_block(keep, j);
+    const bool cand = valid && !forced;
+    const bool tie = cand && key[c] == thr;
+    const uint64_t tie_mask = __ballot(tie);
+    const uint32_t tie_rank = ties + (uint32_t)lanes_below(tie_mask);
+    const bool take = forced || (cand && (key[c] > thr || (tie && tie_rank < take_ties)));
+    const uint64_t take_mask = __ballot(take);
+    if (take) out[pos + lanes_below(take_mask)] = j;
+    pos += __popcll(take_mask);
+    ties += (uint32_t)__popcll(tie_mask);
   }
-  if (lane == 0) a.kv_num_blocks[r] = pos;
+  if (lane == 0) *num_out = pos;
+}
+
+// Rows of up to 64 C blocks: one wave per row reads its row of S straight
+// into registers (coalesced, 256 bytes per load).
+template <int C>
+__global__ __launch_bounds__(64 * kSelWaves) void select_reg_kernel(SelectArgs a) {
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int64_t row = (int64_t)blockIdx.x * kSelWaves + wave;
+  if (row >= a.rows) return;  // wave-uniform; no barrier below
+  const int h = (int)((row / a.n_q) % a.heads);
+  const float* s = a.s + row * a.n_k;
+  // all loads first (in bounds, independent), then the keys
+  float sv[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int j = 64 * c + lane;
+    sv[c] = s[j < a.n_k ? j : a.n_k - 1];
+  }
+  uint32_t key[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int j = 64 * c + lane;
+    key[c] = (j < a.n_k && !keep_block(a.keep, j)) ? order_key(sv[c]) : 0u;
+  }
+  select_row_regs<C>(key, a.n_k, a.budget.k[h], a.keep, lane, a.kv_indices + row * a.stride,
+                     a.kv_num_blocks + row);
+}
+
+// ---------------------------------------------------------------------------
+// Fused scores and selection: S_ij = tau qbar_i . kbar_j (Eq. 2) for the
+// kFusedRows query blocks of one head goes into LDS as order keys, and each
+// wave then selects one row from there (Eq. 6), so S never leaves the CU.
+//
+// Scores on v_mfma_f32_16x16x4_f32 (fp32 products, fp32 accumulation): per
+// 16-key tile, A = kbar (16 keys x 4 d), B = qbar^T (4 d x 16 query blocks),
+// C = S^T (16 keys x 16 query blocks).  Lane l (g = l / 16) supplies
+// A[l % 16][g] and B[g][l % 16], and receives C[4 g + r][l % 16], r = 0..3:
+// four consecutive keys of one row, stored as one 16-byte LDS write.  The d
+// index is permuted consistently between A and B: MFMA s = 4 c + e reads
+// d = 16 c + 4 g + e, so that lane l loads its kbar (and qbar) row as float4 at
+// d = 16 c + 4 g and the four lanes of a row read 64 contiguous bytes per load.
+// The 16-key tiles go round-robin over the waves.  Work-groups are numbered
+// so that each XCD runs consecutive groups of query blocks (one head's kbar
+// at a time in its L2).
+// ---------------------------------------------------------------------------
+template <int D, int C>
+__global__ __launch_bounds__(64 * kFusedRows) void score_select_kernel(ScoreSelectArgs a) {
+  extern __shared__ uint32_t fused_keys[];  // [kFusedRows][row_len] order keys
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int groups = (a.n_q + kFusedRows - 1) / kFusedRows;
+  const int64_t wl = xcd_linear(blockIdx.x, (int64_t)gridDim.x);
+  const int64_t bh = wl / groups;
+  const int i0 = (int)(wl % groups) * kFusedRows;
+  const int row_len = (a.n_k + 15) / 16 * 16;  // whole 16-key tiles
+
+  constexpr int DC = D / 16;  // float4 loads per lane and row (d = 16 c + 4 g)
+  const int n16 = lane % 16, g = lane / 16;
+  // B operand: qbar of query block i0 + n16, zeros past n_q
+  const int qi = i0 + n16;
+  const float* qrow = a.q_bar + (bh * a.n_q + (qi < a.n_q ? qi : 0)) * D;
+  float4 qf[DC];
+#pragma unroll
+  for (int c = 0; c < DC; ++c)
+    qf[c] = qi < a.n_q ? *reinterpret_cast<const float4*>(qrow + 16 * c + 4 * g) : make_float4(0.f, 0.f, 0.f, 0.f);
+
+  const float* kb = a.k_bar + bh * (int64_t)a.n_k * D;
+  const int tiles = row_len / 16;
+  // kbar rows of tile kt (zeros past n_k); the next tile's loads are issued
+  // before the current tile's MFMAs
+  auto load_k = [&](int kt, float4 (&kf)[DC]) {
+    const int kj = kt * 16 + n16;
+    const bool ok = kt < tiles && kj < a.n_k;
+    const float* krow = kb + (int64_t)(ok ? kj : 0) * D;
+#pragma unroll
+    for (int c = 0; c < DC; ++c) {
+      const float4 v = *reinterpret_cast<const float4*>(krow + 16 * c + 4 * g);
+      kf[c] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  float4 kn[DC];
+  load_k(wave, kn);
+  for (int kt = wave; kt < tiles; kt += kFusedRows) {
+    float4 kf[DC];
+#pragma unroll
+    for (int c = 0; c < DC; ++c) kf[c] = kn[c];
+    load_k(kt + kFusedRows, kn);
+    // two independent accumulation chains (even and odd c), added at the end
+    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < DC; c += 2) {
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c].x, qf[c].x, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c + 1].x, qf[c + 1].x, acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c].y, qf[c].y, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c + 1].y, qf[c + 1].y, acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c].z, qf[c].z, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c + 1].z, qf[c + 1].z, acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c].w, qf[c].w, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c + 1].w, qf[c + 1].w, acc1, 0, 0, 0);
+    }
+    const f32x4 acc = acc0 + acc1;
+    // keys 16 kt + 4 g + r of row n16; forced blocks and blocks past n_k get key 0
+    uint32_t k4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = 16 * kt + 4 * g + r;
+      k4[r] = (j < a.n_k && !keep_block(a.keep, j)) ? order_key(a.tau * acc[r]) : 0u;
+    }
+    *reinterpret_cast<uint4*>(fused_keys + (size_t)n16 * row_len + 16 * kt + 4 * g) =
+        make_uint4(k4[0], k4[1], k4[2], k4[3]);
+  }
+  __syncthreads();
+
+  const int i = i0 + wave;
+  if (i >= a.n_q) return;  // wave-uniform; no barrier below
+  const uint32_t* rk = fused_keys + (size_t)wave * row_len;
+  uint32_t key[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int j = 64 * c + lane;
+    const uint32_t v = rk[j < row_len ? j : row_len - 1];  // in bounds, independent reads
+    key[c] = j < a.n_k ? v : 0u;
+  }
+  const int64_t r = bh * a.n_q + i;
+  select_row_regs<C>(key, a.n_k, a.budget.k[(int)(bh % a.heads)], a.keep, lane, a.kv_indices + r * a.stride,
+                     a.kv_num_blocks + r);
+}
+
+size_t score_select_lds_bytes(int n_k) { return (size_t)kFusedRows * ((n_k + 15) / 16 * 16) * sizeof(uint32_t); }
+
+template <int D>
+static hipError_t launch_fused_d(const ScoreSelectArgs& a, int64_t grid, hipStream_t stream) {
+  const size_t lds = score_select_lds_bytes(a.n_k);
+  if (a.n_k <= 512) score_select_kernel<D, 8><<<grid, 64 * kFusedRows, lds, stream>>>(a);
+  else if (a.n_k <= 1024) score_select_kernel<D, 16><<<grid, 64 * kFusedRows, lds, stream>>>(a);
+  else if (a.n_k <= 1536) score_select_kernel<D, 24><<<grid, 64 * kFusedRows, lds, stream>>>(a);
+  else score_select_kernel<D, 36><<<grid, 64 * kFusedRows, lds, stream>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_select(const ScoreSelectArgs& a, hipStream_t stream) {
+  static_assert(kFusedMaxBlocks <= 64 * 36, "fused rows fit the largest register count");
+  static_assert((size_t)kFusedRows * kFusedMaxBlocks * 4 <= 160 * 1024, "fused rows fit in LDS");
+  const int64_t grid = (int64_t)a.bh * ((a.n_q + kFusedRows - 1) / kFusedRows);
+  if (grid == 0) return hipSuccess;
+  if (a.n_k > kFusedMaxBlocks) return hipErrorInvalidValue;
+  if (a.d == 128) return launch_fused_d<128>(a, grid, stream);
+  if (a.d == 64) return launch_fused_d<64>(a, grid, stream);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t grid = (a.rows + kSelWaves - 1) / kSelWaves;
   if (grid == 0) return hipSuccess;
-  if (a.n_k <= kSelCachedMaxBlocks)
-    select_cached_kernel<<<grid, 64 * kSelWaves, (size_t)kSelWaves * ((a.n_k + 3) / 4) * sizeof(uint4), stream>>>(a);
-  else
-    select_kernel<<<grid, 64 * kSelWaves, 0, stream>>>(a);
+  if (a.n_k <= 512) select_reg_kernel<8><<<grid, 64 * kSelWaves, 0, stream>>>(a);
+  else if (a.n_k <= 1024) select_reg_kernel<16><<<grid, 64 * kSelWaves, 0, stream>>>(a);
+  else if (a.n_k <= 1536) select_reg_kernel<24><<<grid, 64 * kSelWaves, 0, stream>>>(a);
+  else if (a.n_k <= 2304) select_reg_kernel<36><<<grid, 64 * kSelWaves, 0, stream>>>(a);
+  else if (a.n_k <= kSelRegMaxBlocks) select_reg_kernel<kSelRegMaxBlocks / 64><<<grid, 64 * kSelWaves, 0, stream>>>(a);
+  else select_kernel<<<grid, 64 * kSelWaves, 0, stream>>>(a);
   return hipGetLastError();
 }
 

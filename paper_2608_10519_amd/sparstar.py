@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libsparstar.so")
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 MAX_KEEP_RANGES = 8
+FUSED_MAX_BLOCKS = 2304  # SPARSTAR_FUSED_MAX_BLOCKS
 MAX_MASS_ROWS = 16
 
 _lib = None
@@ -52,6 +53,9 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.sparstar_score_blocks.argtypes = [c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_dp, c_i, c_rp, c_i,
                                           c_p, c_p, c_i, c_p, c_p, c_sz, c_p]
     lib.sparstar_score_blocks.restype = c_i
+    lib.sparstar_score_blocks_fused.argtypes = [c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_dp, c_i, c_rp, c_i,
+                                                c_p, c_p, c_i, c_p, c_sz, c_p]
+    lib.sparstar_score_blocks_fused.restype = c_i
     lib.sparstar_attn_workspace_bytes.argtypes = [c_i, c_i, c_i64, c_i64, c_i, c_i]
     lib.sparstar_attn_workspace_bytes.restype = c_sz
     lib.sparstar_sparse_attn_fwd.argtypes = [c_p, c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_p, c_p, c_i,
@@ -164,8 +168,11 @@ def sparstar_scale_densities(scale_lq: Sequence[int], finest_rho: Sequence[float
 
 def sparstar_score_blocks(q: torch.Tensor, k: torch.Tensor, block_size: int, budget, keep=(), *,
                           kv_stride: int | None = None, scores: torch.Tensor | None = None,
-                          workspace: torch.Tensor | None = None, out=None):
-    """Selector: returns (kv_num_blocks [B,H,n_q] int32, kv_indices [B,H,n_q,kv_stride] int32)."""
+                          workspace: torch.Tensor | None = None, out=None, fused: bool = False):
+    """Selector: returns (kv_num_blocks [B,H,n_q] int32, kv_indices [B,H,n_q,kv_stride] int32).
+
+    fused=True runs sparstar_score_blocks_fused (scores and selection in one
+    kernel, S kept in LDS; no `scores` output)."""
     B, H, Lq, D = _bhld(q, "q")
     Bk, Hk, Lk, Dk = _bhld(k, "k")
     if (B, H, D) != (Bk, Hk, Dk):
@@ -184,11 +191,20 @@ def sparstar_score_blocks(q: torch.Tensor, k: torch.Tensor, block_size: int, bud
     ws_bytes = sparstar_score_workspace_bytes(B, H, Lq, Lk, D, block_size)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
-    rc = lib.sparstar_score_blocks(q.data_ptr(), k.data_ptr(), B, H, Lq, Lk, D, block_size, bud, nb, kr, nkeep,
-                                   num.data_ptr(), idx.data_ptr(), kv_stride,
-                                   scores.data_ptr() if scores is not None else None,
-                                   workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream())
-    _check("sparstar_score_blocks", rc)
+    ws_n = workspace.numel() * workspace.element_size()
+    if fused:
+        if scores is not None:
+            raise ValueError("the fused selector writes no scores")
+        rc = lib.sparstar_score_blocks_fused(q.data_ptr(), k.data_ptr(), B, H, Lq, Lk, D, block_size, bud, nb, kr,
+                                             nkeep, num.data_ptr(), idx.data_ptr(), kv_stride, workspace.data_ptr(),
+                                             ws_n, _stream())
+        _check("sparstar_score_blocks_fused", rc)
+    else:
+        rc = lib.sparstar_score_blocks(q.data_ptr(), k.data_ptr(), B, H, Lq, Lk, D, block_size, bud, nb, kr, nkeep,
+                                       num.data_ptr(), idx.data_ptr(), kv_stride,
+                                       scores.data_ptr() if scores is not None else None,
+                                       workspace.data_ptr(), ws_n, _stream())
+        _check("sparstar_score_blocks", rc)
     return num, idx
 
 

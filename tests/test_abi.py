@@ -104,6 +104,34 @@ def test_score_blocks_rejects_invalid_arguments(lib, over, code, msg):
     assert msg in S.last_error()
 
 
+def _score_fused(lib, **over):
+    a = dict(q=FAKE, k=FAKE, B=1, H=2, Lq=512, Lk=1152, D=64, block=64, budget=[0.25], keep=[(0, 128)], num=FAKE,
+             idx=FAKE, stride=6, ws=FAKE, ws_bytes=1 << 40)
+    a.update(over)
+    bud = (ctypes.c_double * len(a["budget"]))(*a["budget"])
+    kr = (S.Range * len(a["keep"]))(*[S.Range(x, y) for x, y in a["keep"]])
+    return lib.sparstar_score_blocks_fused(a["q"], a["k"], a["B"], a["H"], a["Lq"], a["Lk"], a["D"], a["block"],
+                                           bud, len(a["budget"]), kr, len(a["keep"]), a["num"], a["idx"],
+                                           a["stride"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("over,code,msg", [
+    (dict(D=96), S.ERR_UNSUPPORTED, "head dim"),
+    (dict(stride=5), S.ERR_INVALID_ARG, "kv_stride"),
+    (dict(ws=None), S.ERR_WORKSPACE, "workspace"),
+    # one key block past the fused kernel's LDS rows
+    (dict(Lk=64 * S.FUSED_MAX_BLOCKS + 1, stride=1000), S.ERR_UNSUPPORTED, "at most 2304"),
+])
+def test_score_blocks_fused_rejects_invalid_arguments(lib, over, code, msg):
+    assert _score_fused(lib, **over) == code
+    assert msg in S.last_error()
+
+
+def test_score_blocks_fused_takes_the_limit_on_an_empty_query_side(lib):
+    # Lq = 0 is a no-op that touches no device memory, after the size checks
+    assert _score_fused(lib, Lq=0, Lk=64 * S.FUSED_MAX_BLOCKS, stride=1000) == S.OK
+
+
 def _attn(lib, dense=False, **over):
     a = dict(q=FAKE, k=FAKE, v=FAKE, B=1, H=2, Lq=512, Lk=1152, D=64, block=64, num=FAKE, idx=FAKE, stride=6,
              scale=0.0, o=FAKE, lse=None, ws=None, ws_bytes=0)

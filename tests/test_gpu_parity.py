@@ -45,7 +45,7 @@ def _times_pow2(bits: np.ndarray, e: int) -> np.ndarray:
     return bf16_bits((bf16_to_f64(bits) * 2.0 ** e).astype(np.float32))
 
 
-def _run_selector(lib, w: Workload, q, k, keep, budget, with_scores=True):
+def _run_selector(lib, w: Workload, q, k, keep, budget, with_scores=True, fused=False):
     import torch
 
     B, H, Lq, D = q.shape
@@ -54,7 +54,7 @@ def _run_selector(lib, w: Workload, q, k, keep, budget, with_scores=True):
     ws = torch.empty(lib.sparstar_score_workspace_bytes(B, H, Lq, Lk, D, w.block), dtype=torch.uint8,
                      device="cuda")
     scores = torch.full((B, H, n_q, n_k), float("nan"), device="cuda") if with_scores else None
-    num, idx = lib.sparstar_score_blocks(q, k, w.block, budget, keep, scores=scores, workspace=ws)
+    num, idx = lib.sparstar_score_blocks(q, k, w.block, budget, keep, scores=scores, workspace=ws, fused=fused)
     torch.cuda.synchronize()
     qb, kb = _ws_views(ws, B, H, n_q, n_k, D)
     return num, idx, scores, qb, kb
@@ -71,26 +71,48 @@ SELECTOR_CASES = [
                                     heads=2, seed=9, density=0.4), 2),
     ("many-tiles", TINY.with_(name="r4", head_dim=128, lq=64 * 70 + 5, l_ref=64 * 60 + 9, l_text=200, heads=2,
                               seed=10, aligned=5, density=0.3), 2),
-    # more than 3584 key blocks: the rows no longer fit the select kernel's LDS cache
+    # rows held in registers at 16 and 24 keys per lane (513-1024 and 1025-1536 key blocks)
+    ("rows-800", TINY.with_(name="r8", heads=1, lq=300, l_ref=64 * 800 - 300 - 128 - 5, l_text=128, seed=14,
+                            density=0.3), 2),
+    ("rows-1300", TINY.with_(name="r9", heads=1, lq=300, l_ref=64 * 1300 - 300 - 128 - 7, l_text=128, seed=15,
+                             density=0.3), 2),
+    # more than 3584 key blocks: the rows no longer fit in registers and stream from memory
     ("long-rows", TINY.with_(name="r5", heads=1, lq=200, l_ref=64 * 3650 + 17, l_text=128, seed=11,
                              density=0.2), 2),
+    # 2304 key blocks, the most the fused score/select kernel keeps in LDS, and one more
+    ("fused-limit", TINY.with_(name="r6", heads=2, lq=64 * 17 + 3, l_ref=64 * 2304 - 64 * 17 - 3 - 128,
+                               l_text=128, seed=12, density=0.2), 2),
+    ("past-fused-limit", TINY.with_(name="r7", heads=1, lq=200, l_ref=64 * 2304 - 200 - 128 + 1, l_text=128,
+                                    seed=13, density=0.2), 2),
 ]
+# long rows crowd the scores together; x8 (exact in bf16) spreads them so that
+# some rows have a clear top-k boundary
+_SPREAD = {"rows-800", "rows-1300", "long-rows", "fused-limit", "past-fused-limit"}
 
 
 @pytest.mark.parametrize("name,w,clip", SELECTOR_CASES, ids=[c[0] for c in SELECTOR_CASES])
 def test_selector_matches_oracle(gpu_lib, name, w, clip):
     _say(f"[selector] {name}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk} clip={clip}")
     qb_, kb_, _ = generate(w)
-    if name == "long-rows":
-        # 3,600 candidates per row crowd the scores together; x8 (exact in bf16)
-        # spreads them so that some rows have a clear top-k boundary
+    if name in _SPREAD:
         qb_, kb_ = _times_pow2(qb_, 3), _times_pow2(kb_, 3)
     keep = keep_ranges(w, clip)
-    num, idx, scores, qbar, kbar = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, w.density)
+    q_d, k_d = to_dev(qb_), to_dev(kb_)
+    # pool, score and select kernels, with S written out and without
+    num, idx, scores, qbar, kbar = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density)
     lists = lists_from_device(num, idx)
+    num_n, idx_n, _, _, _ = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density, with_scores=False)
+    assert lists_from_device(num_n, idx_n) == lists
+    # scores and selection fused (S kept in LDS), up to 2304 key blocks
+    n_k = -(-w.lk // w.block)
+    lists_f = None
+    if n_k <= gpu_lib.FUSED_MAX_BLOCKS:
+        num_f, idx_f, _, _, _ = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density, with_scores=False, fused=True)
+        lists_f = lists_from_device(num_f, idx_f)
     s_gpu = scores.cpu().numpy()
     qbar, kbar = qbar.cpu().numpy(), kbar.cpu().numpy()
     stats = {"exact": 0, "tolerant": 0}
+    stats_f = {"exact": 0, "tolerant": 0}
     for h in range(w.heads):
         q = bf16_to_f64(qb_[0, h])
         k = bf16_to_f64(kb_[0, h])
@@ -102,8 +124,11 @@ def test_selector_matches_oracle(gpu_lib, name, w, clip):
         assert (err <= 1e-5 * (1 + np.abs(s_ref[:, sel]))).all(), f"head {h}: max |dS| {err.max():.3e}"
         for i, row in enumerate(lists[0][h]):
             stats[check_gap_rule(row, s_ref[i], keep_set, sel, kk)] += 1
-    _say(f"[selector] {name}: rows {stats}")
-    assert stats["exact"] > 0
+        if lists_f is not None:
+            for i, row in enumerate(lists_f[0][h]):
+                stats_f[check_gap_rule(row, s_ref[i], keep_set, sel, kk)] += 1
+    _say(f"[selector] {name}: rows {stats}, fused {stats_f if lists_f is not None else 'n/a'}")
+    assert stats["exact"] > 0 and (lists_f is None or stats_f["exact"] > 0)
 
 
 def test_selector_per_head_budgets_and_edge_budgets(gpu_lib):
@@ -154,7 +179,16 @@ def test_selector_ties_prefer_lower_index(gpu_lib):
         # the GPU's own fp32 scores decide; equal scores must resolve to lower indices
         want = sorted(set(keep_set) | set(O.topk_idx(s[i].astype(np.float64), sel, 3)))
         assert row == want, (i, row, want)
-    assert torch.equal(num, num)
+    # the fused kernel computes its own scores (another summation order), but
+    # the copies score equally among themselves: whichever number of them it
+    # takes must be the lowest indices of the group
+    num_f, idx_f, _, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, 3 / 16, with_scores=False,
+                                          fused=True)
+    group = sorted(list(range(0, 4)) + [11] + list(range(12, 16)))
+    for i, row in enumerate(lists_from_device(num_f, idx_f)[0][0]):
+        taken = [j for j in row if j in group]
+        assert taken == group[: len(taken)], (i, row)
+        assert len(row) == len(keep_set) + 3
 
 
 def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_override=None, split=True):
