@@ -648,7 +648,7 @@ void attn_fwd_kernel(AttnArgs a) {
 // Combines the kSplits partial results of one query block:
 //   O = sum_r w_r O_r / sum_r w_r,  w_r = l_r 2^(m_r - M),  M = max_r m_r,
 //   lse = ln2 (M + log2 sum_r w_r).
-// Ranges with no visible key (l_r = 0) have weight 0 and their O_r is not read.
+// Ranges with no visible key (l_r = 0) have weight 0 and their O_r (zeros) add nothing.
 template <int D, int BLK>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   __shared__ float wts[kSplits][BLK];
@@ -684,15 +684,21 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   for (int c = tid; c < BLK * CPR; c += 256) {
     const int row = c / CPR, d0 = (c % CPR) * 8;
     if (row >= rows) continue;
+    // every range's partial is written (zeros when it saw no key), so all
+    // kSplits loads are issued at once; a zero weight then drops its term
+    f16x8 v[kSplits];
+#pragma unroll
+    for (int r = 0; r < kSplits; ++r) {
+      const int64_t prow = (work * kSplits + r) * BLK + row;
+      v[r] = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.part_o) + prow * D + d0);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // the loads stay ahead of their uses
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int r = 0; r < kSplits; ++r) {
       const float w = wts[r][row];
-      if (w == 0.f) continue;
-      const int64_t prow = (work * kSplits + r) * BLK + row;
-      const f16x8 v = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.part_o) + prow * D + d0);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = fmaf(w, (float)v[e], acc[e]);
+      for (int e = 0; e < 8; ++e) acc[e] = w != 0.f ? fmaf(w, (float)v[r][e], acc[e]) : acc[e];
     }
     uint4 o;
     o.x = pack2_bf16(acc[0], acc[1]);
