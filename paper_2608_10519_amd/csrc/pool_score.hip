@@ -37,13 +37,17 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   const int t = threadIdx.x, c = t % CH, g = t / CH;
   const int64_t rows_left = len - (int64_t)blk * BLK;
 
+  // all loads in flight at once (rows past the end re-read the last row, then count as zeros)
   uint4 v[RPT];
 #pragma unroll
   for (int r = 0; r < RPT; ++r) {
     const int row = g + r * RG;
-    v[r] = row < rows_left ? *reinterpret_cast<const uint4*>(src + (int64_t)row * D + c * 8)
-                           : make_uint4(0, 0, 0, 0);
+    const int64_t rr = row < rows_left ? row : rows_left - 1;
+    v[r] = *reinterpret_cast<const uint4*>(src + rr * D + c * 8);
   }
+#pragma unroll
+  for (int r = 0; r < RPT; ++r)
+    if (g + r * RG >= rows_left) v[r] = make_uint4(0, 0, 0, 0);
   float acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.f;
@@ -103,25 +107,40 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   const int t = threadIdx.x;
   const int wave = t / 64, lane = t % 64, l32 = lane % 32, h = lane / 32;
   const int wq = wave / 2, wk = wave % 2;  // the wave's 32 x 32 sub-tile
-  // loader: 64 rows x SKC floats = 512 float4 per tile; thread t loads rows lr and lr + 32
+  // loader: 64 rows x SKC floats = 512 float4 per tile; thread t loads rows lr and lr + 32.
+  // Rows past the end re-read a valid row and are zeroed when staged; the
+  // next chunk's loads are in flight while the current chunk is multiplied.
   const int lr = t / 8, lc = (t % 8) * 4;
-  const bool q_ok[2] = {i0 + lr < a.n_q, i0 + lr + 32 < a.n_q};
-  const bool k_ok[2] = {j0 + lr < a.n_k, j0 + lr + 32 < a.n_k};
+  const bool q0_ok = i0 + lr < a.n_q, q1_ok = i0 + lr + 32 < a.n_q;
+  const bool k0_ok = j0 + lr < a.n_k, k1_ok = j0 + lr + 32 < a.n_k;
+  const float* const qr0 = qb + (int64_t)(q0_ok ? i0 + lr : 0) * D + lc;
+  const float* const qr1 = qb + (int64_t)(q1_ok ? i0 + lr + 32 : 0) * D + lc;
+  const float* const kr0 = kb + (int64_t)(k0_ok ? j0 + lr : 0) * D + lc;
+  const float* const kr1 = kb + (int64_t)(k1_ok ? j0 + lr + 32 : 0) * D + lc;
+  float4 q0 = *reinterpret_cast<const float4*>(qr0), q1 = *reinterpret_cast<const float4*>(qr1);
+  float4 k0 = *reinterpret_cast<const float4*>(kr0), k1 = *reinterpret_cast<const float4*>(kr1);
+  // element-wise (a select of whole float4 values goes through scratch memory)
+  auto keep_if = [](bool ok, float4 v) {
+    return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
+  };
 
   f32x16 acc;
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-  for (int d0 = 0; d0 < D; d0 += SKC) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int row = lr + 32 * u;
-      float4 qv = make_float4(0.f, 0.f, 0.f, 0.f), kv = qv;
-      if (q_ok[u]) qv = *reinterpret_cast<const float4*>(qb + (int64_t)(i0 + row) * D + d0 + lc);
-      if (k_ok[u]) kv = *reinterpret_cast<const float4*>(kb + (int64_t)(j0 + row) * D + d0 + lc);
-      *reinterpret_cast<float4*>(qs + row * RS + lc) = qv;
-      *reinterpret_cast<float4*>(ks + row * RS + lc) = kv;
-    }
+  for (int d0 = 0; d0 < D; d0 += SKC) {
+    if (d0 > 0) __syncthreads();  // the previous chunk's reads are done
+    *reinterpret_cast<float4*>(qs + lr * RS + lc) = keep_if(q0_ok, q0);
+    *reinterpret_cast<float4*>(qs + (lr + 32) * RS + lc) = keep_if(q1_ok, q1);
+    *reinterpret_cast<float4*>(ks + lr * RS + lc) = keep_if(k0_ok, k0);
+    *reinterpret_cast<float4*>(ks + (lr + 32) * RS + lc) = keep_if(k1_ok, k1);
     __syncthreads();
+    if (d0 + SKC < D) {
+      q0 = *reinterpret_cast<const float4*>(qr0 + d0 + SKC);
+      q1 = *reinterpret_cast<const float4*>(qr1 + d0 + SKC);
+      k0 = *reinterpret_cast<const float4*>(kr0 + d0 + SKC);
+      k1 = *reinterpret_cast<const float4*>(kr1 + d0 + SKC);
+    }
     const float* qa = qs + (wq * 32 + l32) * RS + (SKC / 2) * h;
     const float* kc = ks + (wk * 32 + l32) * RS + (SKC / 2) * h;
 #pragma unroll
@@ -133,7 +152,6 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.z, y.z, acc, 0, 0, 0);
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.w, y.w, acc, 0, 0, 0);
     }
-    __syncthreads();
   }
 
   const int j = j0 + wk * 32 + l32;
