@@ -25,7 +25,8 @@ def _say(msg):
     sys.stdout.flush()
 
 
-def _run_full(lib, w, budget):
+def _run_full(lib, w, budget, fused=None):
+    """fused: a list that receives the fused selector's (num, idx) as well."""
     import torch
 
     _say(f"[full] {w.name}: generating H={w.heads} Lq={w.lq} Lk={w.lk}")
@@ -35,6 +36,10 @@ def _run_full(lib, w, budget):
     _say(f"[full] {w.name}: selector + sparse forward on the GPU")
     num, idx = lib.sparstar_score_blocks(q, k, w.block, budget, keep)
     o, lse = lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
+    if fused is not None:
+        _say(f"[full] {w.name}: fused score/select on the GPU")
+        nf, xf = lib.sparstar_score_blocks(q, k, w.block, budget, keep, fused=True)
+        fused.extend([nf.cpu().numpy(), xf.cpu().numpy()])
     torch.cuda.synchronize()
     return (qb, kb, vb), keep, num.cpu().numpy(), idx.cpu().numpy(), o.float().cpu().numpy(), lse.cpu().numpy()
 
@@ -72,11 +77,24 @@ def test_mid_scale_parity(gpu_lib):
 
 def test_720p_final_scale_parity(gpu_lib):
     w = P720
-    data, keep, num, idx, o, lse = _run_full(gpu_lib, w, w.density)
+    fused = []
+    data, keep, num, idx, o, lse = _run_full(gpu_lib, w, w.density, fused=fused)
     n_q = -(-w.lq // w.block)
     assert (num == 8 + 563).all()
     _check_heads(w, data, keep, num, idx, o, lse, heads=[0, 17], qblocks=[0, 561, n_q - 1],
                  budgets=np.full(w.heads, w.density))
+    # the fused score/select kernel on the same inputs: every row of head 5 under the gap rule
+    nf, xf = fused
+    assert (nf == 8 + 563).all()
+    qb, kb, _ = data
+    h = 5
+    _say(f"[full] {w.name}: oracle selector head {h} for the fused kernel")
+    _, s_ref, kk, keep_set = O.select(bf16_to_f64(qb[0, h]), bf16_to_f64(kb[0, h]), w.block, w.density, keep)
+    sel = O.selectable_blocks(keep_set, w.lk, w.block)
+    stats = {"exact": 0, "tolerant": 0}
+    for i in range(n_q):
+        stats[check_gap_rule(xf[0, h, i, : nf[0, h, i]].tolist(), s_ref[i], keep_set, sel, kk)] += 1
+    _say(f"[full] {w.name}: fused head {h} rows {stats}")
 
 
 def test_720p_per_head_budget_sweep_parity(gpu_lib):
