@@ -134,8 +134,8 @@ def budget_k(rho: float, n_sel: int) -> int:
     """k = min(n_sel, max(1, ceil(rho * n_sel)))  (Eq. 5).
 
     Reading of the ceiling: rho arrives as a double; when rho*n_sel lies within
-    1e-9*max(1, n_sel) of an integer, that integer is taken (so 10% of 2,250 is
-    225, as intended, not 226 from the binary representation of 0.1); otherwise
+    1e-9*max(1, n_sel) of an integer, that integer is taken (so 14% of 2,250 is
+    315, as intended, not 316 from the binary representation of 0.14); otherwise
     the ceiling of the double product.  n_sel = 0 gives k = 0."""
     if not (0.0 <= rho <= 1.0) or math.isnan(rho):
         raise ValueError("density must lie in [0, 1]")

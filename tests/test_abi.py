@@ -49,6 +49,7 @@ def test_workspace_bytes(lib):
 @pytest.mark.parametrize("H,Lk,b,budget,keep,want", [
     (24, 144_512, 64, 0.25, [(72_000, 72_512)], 8 + 563),
     (24, 144_512, 64, 0.10, [(72_000, 72_512)], 8 + 225),
+    (24, 144_512, 64, 0.14, [(72_000, 72_512)], 8 + 315),       # 0.14 * 2250 = 315.00000000000006 in binary
     (24, 144_512, 128, 0.25, [(72_000, 72_512)], 5 + 281),      # n_k = 1129, 5 straddling text blocks, n_sel 1124
     (2, 1152, 64, 0.25, [(512, 640)], 2 + 4),
     (2, 1152, 64, 0.25, [(512, 640), (0, 512)], 10 + 2),         # clip 1: text + reference

@@ -116,6 +116,9 @@ BUDGET_TABLE = [
     (0.0, 1, 1), (0.5, 1, 1), (1.0, 1, 1),
     (0.0, 0, 0), (0.5, 0, 0), (1.0, 0, 0),
     (0.25, 1305, 327), (0.7, 10, 7), (0.3, 10, 3),
+    # products a hair above an integer in binary (0.14 * 2250 = 315.00000000000006):
+    # the exact decimal product is an integer, so that integer is k
+    (0.14, 2250, 315), (0.28, 2250, 630), (0.07, 100, 7), (0.55, 100, 55),
 ]
 
 
