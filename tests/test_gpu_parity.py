@@ -425,6 +425,17 @@ def test_deterministic(gpu_lib):
             c = int(n[0, h, i])
             assert torch.equal(i1[0, h, i, :c], i2[0, h, i, :c])
     assert torch.equal(o1[0], o2[0]) and torch.equal(o1[1], o2[1])
+    # the fused selector too
+    f1 = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep, fused=True)
+    f2 = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep, fused=True)
+    torch.cuda.synchronize()
+    assert torch.equal(f1[0], f2[0])
+    nf = f1[0].cpu()
+    j1, j2 = f1[1].cpu(), f2[1].cpu()
+    for h in range(w.heads):
+        for i in range(nf.shape[2]):
+            c = int(nf[0, h, i])
+            assert torch.equal(j1[0, h, i, :c], j2[0, h, i, :c])
 
 
 def test_empty_query_sequence_is_noop(gpu_lib):
