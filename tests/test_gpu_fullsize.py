@@ -5,6 +5,8 @@ All 24 heads run through the C ABI in the launch configuration the benchmark
 times (key-range split with a workspace); the float64 oracle then recomputes
 the selector of sampled heads completely (every row checked under the gap
 rule) and the forward of sampled query blocks (first, last and interior ones).
+At the 720p headline shape every head's forward is checked on four query
+blocks, and six heads' selectors on every row.
 """
 from __future__ import annotations
 
@@ -44,22 +46,22 @@ def _run_full(lib, w, budget, fused=None):
     return (qb, kb, vb), keep, num.cpu().numpy(), idx.cpu().numpy(), o.float().cpu().numpy(), lse.cpu().numpy()
 
 
-def _check_heads(w, data, keep, num, idx, o, lse, heads, qblocks, budgets):
+def _check_heads(w, data, keep, num, idx, o, lse, heads, qblocks, budgets, selector=True):
+    """selector=False checks only the forward (on the GPU's own lists)."""
     qb, kb, vb = data
     n_q = -(-w.lq // w.block)
     for h in heads:
         qh, kh, vh = bf16_to_f64(qb[0, h]), bf16_to_f64(kb[0, h]), bf16_to_f64(vb[0, h])
-        rho = float(budgets[h])
-        _say(f"[full] {w.name}: oracle selector head {h} (rho={rho:.4f})")
-        lists_ref, s_ref, kk, keep_set = O.select(qh, kh, w.block, rho, keep)
-        sel = O.selectable_blocks(keep_set, w.lk, w.block)
-        stats = {"exact": 0, "tolerant": 0}
-        gpu_lists = []
-        for i in range(n_q):
-            row = idx[0, h, i, : num[0, h, i]].tolist()
-            stats[check_gap_rule(row, s_ref[i], keep_set, sel, kk)] += 1
-            gpu_lists.append(row)
-        _say(f"[full] {w.name}: head {h} rows {stats}")
+        gpu_lists = [idx[0, h, i, : num[0, h, i]].tolist() for i in range(n_q)]
+        if selector:
+            rho = float(budgets[h])
+            _say(f"[full] {w.name}: oracle selector head {h} (rho={rho:.4f})")
+            lists_ref, s_ref, kk, keep_set = O.select(qh, kh, w.block, rho, keep)
+            sel = O.selectable_blocks(keep_set, w.lk, w.block)
+            stats = {"exact": 0, "tolerant": 0}
+            for i in range(n_q):
+                stats[check_gap_rule(gpu_lists[i], s_ref[i], keep_set, sel, kk)] += 1
+            _say(f"[full] {w.name}: head {h} rows {stats}")
         for i in qblocks:
             rows = slice(i * w.block, min((i + 1) * w.block, w.lq))
             o_ref, l_ref = O.sparse_attention(qh[rows], kh, vh, [gpu_lists[i]], w.block)
@@ -81,8 +83,12 @@ def test_720p_final_scale_parity(gpu_lib):
     data, keep, num, idx, o, lse = _run_full(gpu_lib, w, w.density, fused=fused)
     n_q = -(-w.lq // w.block)
     assert (num == 8 + 563).all()
-    _check_heads(w, data, keep, num, idx, o, lse, heads=[0, 17], qblocks=[0, 561, n_q - 1],
-                 budgets=np.full(w.heads, w.density))
+    # every head: four query blocks of the forward, stratified so that the first and last blocks are always
+    # checked and the other two move across the sequence; every fifth head also all its selector rows
+    for h in range(w.heads):
+        qblocks = [0, n_q - 1, (47 * h + 11) % n_q, (47 * h + 573) % n_q]
+        _check_heads(w, data, keep, num, idx, o, lse, heads=[h], qblocks=qblocks,
+                     budgets=np.full(w.heads, w.density), selector=h % 5 == 0 or h == w.heads - 1)
     # the fused score/select kernel on the same inputs: every row of head 5 under the gap rule
     nf, xf = fused
     assert (nf == 8 + 563).all()
