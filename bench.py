@@ -74,6 +74,18 @@ def traffic_from_profile() -> dict | None:
     return {"fetch": float(m_f.group(1)), "write": float(m_w.group(1))}
 
 
+def _cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo where there is one)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 def cpu_baseline(w, qb, kb, vb, keep, total_flops: float, lists_gpu) -> dict:
     """Time the oracle on head 0: the whole selector for that head, plus the
     attention of a sample of query blocks; scale to all heads and blocks."""
@@ -108,7 +120,7 @@ def cpu_baseline(w, qb, kb, vb, keep, total_flops: float, lists_gpu) -> dict:
         "kind": "oracle",
         "sample": (f"head 0 of 24: full selector ({n_q} rows, {t_sel:.1f} s) + attention of {len(sample)} "
                    f"evenly spaced query blocks ({t_att:.3f} s each), scaled to 24 heads x {n_q} blocks"),
-        "cpu": platform.processor() or platform.machine(),
+        "cpu": _cpu_model(),
         "lists_equal_gpu_head0": agree,
     }
 
