@@ -256,7 +256,7 @@ def main() -> int:
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported (the hot path shards "
-              "by head with no exchange, but this build measures one GPU only)", file=sys.stderr)
+              "by head with no exchange between GPUs; the benchmark measures one GPU)", file=sys.stderr)
         return 2
 
     if args.copy_calibration:
