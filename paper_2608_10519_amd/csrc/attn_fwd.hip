@@ -649,15 +649,60 @@ void attn_fwd_kernel(AttnArgs a) {
 //   O = sum_r w_r O_r / sum_r w_r,  w_r = l_r 2^(m_r - M),  M = max_r m_r,
 //   lse = ln2 (M + log2 sum_r w_r).
 // Ranges with no visible key (l_r = 0) have weight 0 and their O_r (zeros) add nothing.
+// One thread per 8-column chunk of the query block's rows (two chunks per
+// thread at BLK = 128, D = 128).  Every thread issues the kSplits partial loads
+// of its first chunk before the weights are computed, so that their latency
+// overlaps that of the (max, sum) pairs.
 template <int D, int BLK>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+struct MergeCfg {
+  static constexpr int CPR = D / 8;                     // 8-column chunks per row
+  static constexpr int CHUNKS = BLK * CPR;
+  static constexpr int NT = CHUNKS < 1024 ? CHUNKS : 1024;
+  static constexpr int CPT = CHUNKS / NT;               // chunks per thread
+  static_assert(CPT * NT == CHUNKS && NT >= BLK, "chunk split");
+};
+
+template <int D, int BLK>
+__global__ __launch_bounds__((MergeCfg<D, BLK>::NT)) void attn_merge_kernel(AttnArgs a) {
+  using M = MergeCfg<D, BLK>;
   __shared__ float wts[kSplits][BLK];
   const int64_t work = blockIdx.x;
   const int64_t bh = work / a.n_q;
   const int qb = (int)(work % a.n_q);
   const int tid = threadIdx.x;
   const int64_t rows = a.lq - (int64_t)qb * BLK;
-  for (int row = tid; row < BLK; row += 256) {
+  // every range's partial is written for every row of the block (zeros when it
+  // saw no key), so the loads need no guard; a zero weight drops the term
+  auto load_chunk = [&](int c, f16x8* v) {
+    const int row = c / M::CPR, d0 = (c % M::CPR) * 8;
+#pragma unroll
+    for (int r = 0; r < kSplits; ++r) {
+      const int64_t prow = (work * kSplits + r) * BLK + row;
+      v[r] = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.part_o) + prow * D + d0);
+    }
+  };
+  auto combine = [&](int c, const f16x8* v) {
+    const int row = c / M::CPR, d0 = (c % M::CPR) * 8;
+    if (row >= rows) return;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < kSplits; ++r) {
+      const float w = wts[r][row];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = w != 0.f ? fmaf(w, (float)v[r][e], acc[e]) : acc[e];
+    }
+    uint4 o;
+    o.x = pack2_bf16(acc[0], acc[1]);
+    o.y = pack2_bf16(acc[2], acc[3]);
+    o.z = pack2_bf16(acc[4], acc[5]);
+    o.w = pack2_bf16(acc[6], acc[7]);
+    *reinterpret_cast<uint4*>(a.o + (bh * a.lq + (int64_t)qb * BLK + row) * D + d0) = o;
+  };
+
+  f16x8 v[kSplits];
+  load_chunk(tid, v);
+  if (tid < BLK) {
+    const int row = tid;
     float m[kSplits], l[kSplits], mm = -INFINITY;
 #pragma unroll
     for (int r = 0; r < kSplits; ++r) {
@@ -680,32 +725,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
       a.lse[bh * a.lq + (int64_t)qb * BLK + row] = tot > 0.f ? (mm + log2f(tot)) * 0.69314718055994530942f : -INFINITY;
   }
   __syncthreads();
-  constexpr int CPR = D / 8;
-  for (int c = tid; c < BLK * CPR; c += 256) {
-    const int row = c / CPR, d0 = (c % CPR) * 8;
-    if (row >= rows) continue;
-    // every range's partial is written (zeros when it saw no key), so all
-    // kSplits loads are issued at once; a zero weight then drops its term
-    f16x8 v[kSplits];
+  combine(tid, v);
 #pragma unroll
-    for (int r = 0; r < kSplits; ++r) {
-      const int64_t prow = (work * kSplits + r) * BLK + row;
-      v[r] = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.part_o) + prow * D + d0);
-    }
-    __builtin_amdgcn_sched_barrier(0);  // the loads stay ahead of their uses
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int r = 0; r < kSplits; ++r) {
-      const float w = wts[r][row];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = w != 0.f ? fmaf(w, (float)v[r][e], acc[e]) : acc[e];
-    }
-    uint4 o;
-    o.x = pack2_bf16(acc[0], acc[1]);
-    o.y = pack2_bf16(acc[2], acc[3]);
-    o.z = pack2_bf16(acc[4], acc[5]);
-    o.w = pack2_bf16(acc[6], acc[7]);
-    *reinterpret_cast<uint4*>(a.o + (bh * a.lq + (int64_t)qb * BLK + row) * D + d0) = o;
+  for (int k = 1; k < M::CPT; ++k) {
+    load_chunk(tid + k * M::NT, v);
+    combine(tid + k * M::NT, v);
   }
 }
 
@@ -719,7 +743,7 @@ static hipError_t launch_cfg(const AttnArgs& a, bool dense, hipStream_t stream) 
     else attn_fwd_kernel<D, BLK, false, true><<<items * kSplits, NT, 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    attn_merge_kernel<D, BLK><<<items, 256, 0, stream>>>(a);
+    attn_merge_kernel<D, BLK><<<items, MergeCfg<D, BLK>::NT, 0, stream>>>(a);
   } else {
     if (dense) attn_fwd_kernel<D, BLK, true, false><<<items, NT, 0, stream>>>(a);
     else attn_fwd_kernel<D, BLK, false, false><<<items, NT, 0, stream>>>(a);
