@@ -127,3 +127,59 @@ def test_720p_block_128_parity(gpu_lib):
     assert (num == 5 + O.budget_k(w.density, n_k - 5)).all()
     _check_heads(w, data, keep, num, idx, o, lse, heads=[0, 11], qblocks=[0, 281, n_q - 1],
                  budgets=np.full(w.heads, w.density))
+
+
+def test_pyramid_dense_scale_parity(gpu_lib):
+    """The clip pyramid's first scale (2,880 queries against 75,392 keys) on the
+    dense forward, as the pyramid runs it: sampled query blocks of three heads
+    against the oracle's dense softmax attention."""
+    import torch
+
+    from synthetic import pyramid_scales
+
+    w, sparse = pyramid_scales()[0]
+    assert not sparse
+    heads = [0, 9, 23]
+    _say(f"[full] {w.name}: generating heads {heads} Lq={w.lq} Lk={w.lk}")
+    qb, kb, vb = generate(w, heads=heads, workers=1)
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    o, lse = gpu_lib.sparstar_dense_attn_fwd(q, k, v, w.block)
+    torch.cuda.synchronize()
+    o, lse = o.float().cpu().numpy(), lse.cpu().numpy()
+    n_q = -(-w.lq // w.block)
+    for hi, h in enumerate(heads):
+        qh, kh, vh = bf16_to_f64(qb[0, hi]), bf16_to_f64(kb[0, hi]), bf16_to_f64(vb[0, hi])
+        for i in (0, 17, n_q - 1):
+            rows = slice(i * w.block, min((i + 1) * w.block, w.lq))
+            _say(f"[full] {w.name}: oracle dense head {h} block {i}")
+            o_ref, l_ref = O.dense_attention(qh[rows], kh, vh)
+            check_output(o[0, hi, rows][None].astype(np.float64), o_ref[None],
+                         lse[0, hi, rows][None].astype(np.float64), l_ref[None], what=f"{w.name} head {h} block {i}")
+
+
+def test_pyramid_sparse_scale_parity(gpu_lib):
+    """The clip pyramid's fourth scale (46,080 queries against 118,592 keys,
+    fresh selection at 25%), two heads: every selector row of one head under
+    the gap rule and sampled query blocks of the forward."""
+    from synthetic import pyramid_scales
+
+    w, sparse = pyramid_scales()[3]
+    assert sparse
+    heads = [2, 21]
+    _say(f"[full] {w.name}: generating heads {heads} Lq={w.lq} Lk={w.lk}")
+    qb, kb, vb = generate(w, heads=heads, workers=1)
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    keep = keep_ranges(w)
+    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
+    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
+    import torch
+
+    torch.cuda.synchronize()
+    num, idx = num.cpu().numpy(), idx.cpu().numpy()
+    o, lse = o.float().cpu().numpy(), lse.cpu().numpy()
+    n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
+    assert (num == 8 + O.budget_k(w.density, n_k - 8)).all()
+    _check_heads(w, (qb, kb, vb), keep, num, idx, o, lse, heads=[0], qblocks=[0, 333, n_q - 1],
+                 budgets=np.full(len(heads), w.density))
+    _check_heads(w, (qb, kb, vb), keep, num, idx, o, lse, heads=[1], qblocks=[5, n_q - 2],
+                 budgets=np.full(len(heads), w.density), selector=False)
