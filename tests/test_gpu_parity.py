@@ -146,6 +146,50 @@ def test_selector_per_head_budgets_and_edge_budgets(gpu_lib):
             check_gap_rule(row, s_ref[i], keep_set, sel, kk)
 
 
+def test_selector_eight_keep_ranges(gpu_lib):
+    """The most keep ranges the ABI takes (8), scattered, some straddling block
+    boundaries and one touching the ragged last block."""
+    w = TINY.with_(name="keep8", heads=2, lq=300, l_ref=64 * 40 + 5, l_text=128, seed=23, density=0.3)
+    _say(f"[selector] eight keep ranges: Lk={w.lk}")
+    qb_, kb_, _ = generate(w)
+    lk = w.lk
+    keep = [(0, 10), (130, 140), (250, 390), (700, 700), (1000, 1090), (1500, 1540), (2000, 2100),
+            (lk - 3, lk)]
+    q_d, k_d = to_dev(qb_), to_dev(kb_)
+    for fused in (False, True):
+        num, idx, _, _, _ = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density, with_scores=False, fused=fused)
+        lists = lists_from_device(num, idx)
+        for h in range(w.heads):
+            _, s_ref, kk, keep_set = O.select(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), w.block, w.density,
+                                              keep)
+            sel = O.selectable_blocks(keep_set, w.lk, w.block)
+            for i, row in enumerate(lists[0][h]):
+                check_gap_rule(row, s_ref[i], keep_set, sel, kk)
+
+
+def test_selector_256_heads_with_per_head_budgets(gpu_lib):
+    """The most heads the ABI takes (256), each with its own budget: the
+    per-head budget table indexes by head through the whole range."""
+    w = TINY.with_(name="h256", heads=256, head_dim=64, lq=128, l_ref=64 * 6, l_text=64, seed=29, density=0.5)
+    _say("[selector] 256 heads, per-head budgets")
+    qb_, kb_, _ = generate(w)
+    n_k = -(-w.lk // w.block)
+    keep = keep_ranges(w)
+    budgets = [(h % 9) / 8 for h in range(w.heads)]  # 0, 1/8, ..., 1 repeating
+    num, idx, _, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, budgets, with_scores=False)
+    num = num.cpu().numpy()
+    keep_set = O.keep_blocks(keep, w.lk, w.block)
+    n_sel = n_k - len(keep_set)
+    for h in range(w.heads):
+        assert (num[0, h] == len(keep_set) + O.budget_k(budgets[h], n_sel)).all(), h
+    for h in (0, 7, 8, 100, 255):
+        _, s_ref, kk, ks = O.select(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), w.block, budgets[h], keep)
+        sel = O.selectable_blocks(ks, w.lk, w.block)
+        rows = idx[0, h].cpu().numpy()
+        for i in range(rows.shape[0]):
+            check_gap_rule(rows[i, : num[0, h, i]].tolist(), s_ref[i], ks, sel, kk)
+
+
 def test_selector_everything_forced(gpu_lib):
     """n_sel = 0: every list is exactly J_keep."""
     import torch
