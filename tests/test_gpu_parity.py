@@ -190,6 +190,38 @@ def test_selector_256_heads_with_per_head_budgets(gpu_lib):
             check_gap_rule(rows[i, : num[0, h, i]].tolist(), s_ref[i], ks, sel, kk)
 
 
+@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
+def test_batch_of_two_end_to_end(gpu_lib, split):
+    """B = 2 with per-head budgets: selector (separate and fused) and sparse
+    forward per (batch, head) against the oracle."""
+    import torch
+
+    w = TINY.with_(name="b2", batch=2, heads=3, head_dim=128, lq=64 * 9 + 7, l_ref=64 * 20 + 1, l_text=128,
+                   seed=37, density=0.3)
+    _say(f"[batch] B={w.batch} H={w.heads} Lq={w.lq} Lk={w.lk} split={split}")
+    qb_, kb_, vb_ = generate(w)
+    q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
+    keep = keep_ranges(w)
+    budgets = [0.2, 0.3, 0.45]
+    n_q = -(-w.lq // w.block)
+    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, budgets, keep)
+    nf, xf = gpu_lib.sparstar_score_blocks(q, k, w.block, budgets, keep, fused=True)
+    o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, split=split)
+    torch.cuda.synchronize()
+    lists, lists_f = lists_from_device(num, idx), lists_from_device(nf, xf)
+    og, lg = bf16_tensor_to_f64(o), lse.cpu().numpy().astype(np.float64)
+    for b in range(w.batch):
+        for h in range(w.heads):
+            qh, kh, vh = (bf16_to_f64(x[b, h]) for x in (qb_, kb_, vb_))
+            _, s_ref, kk, keep_set = O.select(qh, kh, w.block, budgets[h], keep)
+            sel = O.selectable_blocks(keep_set, w.lk, w.block)
+            for i in range(n_q):
+                check_gap_rule(lists[b][h][i], s_ref[i], keep_set, sel, kk)
+                check_gap_rule(lists_f[b][h][i], s_ref[i], keep_set, sel, kk)
+            o_ref, l_ref = O.sparse_attention(qh, kh, vh, lists[b][h], w.block)
+            check_output(og[b, h][None], o_ref[None], lg[b, h][None], l_ref[None], what=f"b {b} h {h}")
+
+
 def test_selector_everything_forced(gpu_lib):
     """n_sel = 0: every list is exactly J_keep."""
     import torch
