@@ -23,13 +23,14 @@ def _say(msg):
     sys.stdout.flush()
 
 
-@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
-def test_graph_replay_matches_eager(gpu_lib, split):
+@pytest.mark.parametrize("split,fused", [(True, False), (False, False), (True, True)],
+                         ids=["split", "onepass", "split-fused-selector"])
+def test_graph_replay_matches_eager(gpu_lib, split, fused):
     import torch
 
     S = gpu_lib
     w = TINY.with_(name="graph", head_dim=128, lq=64 * 40 + 9, l_ref=64 * 30 + 3, l_text=150, heads=3, seed=31)
-    _say(f"[graph] H={w.heads} D={w.head_dim} Lq={w.lq} Lk={w.lk} split={split}")
+    _say(f"[graph] H={w.heads} D={w.head_dim} Lq={w.lq} Lk={w.lk} split={split} fused={fused}")
     qb, kb, vb = generate(w)
     q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
     keep = keep_ranges(w)
@@ -46,7 +47,8 @@ def test_graph_replay_matches_eager(gpu_lib, split):
     lse = torch.empty((B, H, Lq), dtype=torch.float32, device="cuda")
 
     def step():
-        S.sparstar_score_blocks(q, k, w.block, w.density, keep, kv_stride=stride, workspace=ws, out=(num, idx))
+        S.sparstar_score_blocks(q, k, w.block, w.density, keep, kv_stride=stride, workspace=ws, out=(num, idx),
+                                fused=fused)
         S.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, out=o, lse=lse, split=split, workspace=aws)
 
     step()
