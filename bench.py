@@ -238,7 +238,7 @@ def attention_mass(r: "Runner", S, torch) -> dict:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--density", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
