@@ -143,9 +143,13 @@ int sparstar_score_blocks_fused(const void* q, const void* k, int B, int H, int6
  * blocks of every query block into 16 contiguous ranges (two per XCD of the
  * MI355X, taken one after the other, so that each XCD's L2 streams about one
  * sixteenth of a head's K/V at a time) and merge the partial results: per
- * (batch, head, query block, range, query row) an fp16 partial O normalised by
- * its own row sum ([.., D]) and an fp32 (running max, row sum) pair.  0 when
- * the key sequence has fewer than 16 blocks (no split), and for invalid sizes.
+ * (batch, head, query block, range, query row) the range's unnormalised
+ * partial P V in fp16, scaled by a power of two chosen per row so that its
+ * largest magnitude lies in [0.5, 1) ([.., D]; any finite bf16 range of V keeps
+ * fp16's relative precision), and four fp32 values (running max, the row sums
+ * of the bf16-rounded and of the unrounded softmax numerators, the row's
+ * scale exponent).  0 when the key sequence has fewer than 16 blocks (no
+ * split), and for invalid sizes.
  */
 size_t sparstar_attn_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size);
 
@@ -156,7 +160,10 @@ size_t sparstar_attn_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D
  *   O_t   = sum_u softmax_u(s * q_t . k_u) v_u   (bf16 out, fp32 accumulation)
  *   lse_t = ln sum_u exp(s * q_t . k_u)          (fp32, natural log)
  * with s = softmax_scale, or D^-1/2 when softmax_scale <= 0.  A row whose list is
- * empty gets O = 0 and lse = -inf.
+ * empty gets O = 0 and lse = -inf.  The softmax weights applied to V are
+ * rounded to bf16 and O is normalised by their sum, so they sum to one exactly
+ * (V = 1 gives O = 1); lse is taken from the sum of the unrounded fp32
+ * weights.  Rows t >= Lq of a partial last query block are never written.
  *
  *   q, k, v         device bf16 Q [B,H,Lq,D], K and V [B,H,Lk,D].
  *   D, block_size   as for sparstar_score_blocks.
@@ -171,7 +178,9 @@ size_t sparstar_attn_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D
  *   workspace       NULL for a single pass, or device scratch of at least
  *                   sparstar_attn_workspace_bytes(...) bytes (256-byte aligned,
  *                   no initialisation needed, garbage afterwards) for the
- *                   key-range split; the results agree to fp32/fp16 rounding.
+ *                   key-range split.  The two paths round P relative to
+ *                   different running maxima, so O agrees to the bf16 rounding
+ *                   of P and O and lse to fp32 rounding.
  */
 int sparstar_sparse_attn_fwd(const void* q, const void* k, const void* v, int B, int H, int64_t Lq, int64_t Lk,
                              int D, int block_size, const int32_t* kv_num_blocks, const int32_t* kv_indices,

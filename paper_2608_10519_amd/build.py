@@ -28,9 +28,14 @@ FLAGS = [
 ]
 
 
+# Every kernel must run without a private (scratch) segment: a register spill to
+# scratch memory is a build error, not a silent slowdown.
+DEVICE_FLAGS = ["-Xarch_device", "-Wframe-larger-than=0", "-Xarch_device", "-Werror=frame-larger-than"]
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    lang = ["-x", "hip"] if src.endswith(".hip") else []
+    lang = ["-x", "hip", *DEVICE_FLAGS] if src.endswith(".hip") else []
     cmd = [HIPCC, *FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:

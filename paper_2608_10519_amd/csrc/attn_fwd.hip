@@ -29,7 +29,8 @@
 //     transpose read ds_read_b64_tr_b16 (in each 16-lane group, source lane s
 //     points at V[r0 + s/4][4 (c0 + s%4)], and lane j receives
 //     V[r0 .. r0+3][4 c0 + j]: 4 keys of one d column).
-// O = O^T / l in bf16, lse = ln2*(m + log2 l).
+// O = O^T / l in bf16 with l the row sum of the bf16-rounded P, and
+// lse = ln2*(m + log2 le) with le the row sum of the unrounded fp32 p.
 //
 // MFMA layouts (v_mfma_f32_32x32x16_bf16, lane l, h = l / 32):
 //   A[m][k]: m = l % 32, k = 8h + i (i = 0..7 of the lane's bf16x8)
@@ -287,7 +288,12 @@ void attn_fwd_kernel(AttnArgs a) {
     if (j >= ntiles) return -1;
     const int e = j / C::SUB, sub = j % C::SUB;
     if constexpr (DENSE) {
-      return (blk_lo + e) * C::SUB + sub;
+      int kt = (blk_lo + e) * C::SUB + sub;
+      // At 128-row blocks the tile index is hidden from the compiler, which
+      // would otherwise precompute the addresses of all six unrolled steps and
+      // spill registers to scratch.
+      if constexpr (BLK == 128) asm volatile("" : "+s"(kt));
+      return kt;
     } else {
       if (e >= lbase + 64) load_batch(lbase + 64);
       const int b = __builtin_amdgcn_readlane(lreg, e - lbase);
@@ -301,7 +307,13 @@ void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc_o[t][e] = 0.f;
   float m_run = -INFINITY;  // running max (log2 domain), shared by both lane halves
-  float l_run = 0.f;        // this lane's partial row sum of the bf16 P it applied
+  // Two row sums per lane (each over the lane's half of the keys):
+  //   l_run:  of the bf16-rounded P that multiplies V, so that O = (P V) / l_run
+  //           is an exact convex combination of the rounded weights (V = 1 gives
+  //           O = 1 exactly);
+  //   le_run: of the unrounded fp32 p, for the log-sum-exp.
+  float l_run = 0.f;
+  float le_run = 0.f;
 
   // ---- direct-to-LDS tile loads: load i of wave w fills LDS bytes
   // [(DPW w + i) KB, +1 KB); lane l writes 16 bytes at +16 l, i.e. physical
@@ -422,6 +434,7 @@ void attn_fwd_kernel(AttnArgs a) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
+      le_run *= alpha;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t)
 #pragma unroll
@@ -476,6 +489,7 @@ void attn_fwd_kernel(AttnArgs a) {
       f32x16 acc_n[C::KT];
       const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
       uint32_t pk[C::KT][8];  // bf16 pairs of P^T, per 32-key sub-tile
+      float pf[C::KT][16];    // the same p in fp32, summed for lse in phase B (one sub-tile per step)
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt) {
         uint4 kf[C::DS];
@@ -492,19 +506,32 @@ void attn_fwd_kernel(AttnArgs a) {
           const float p0 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
           const float p1 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
           pk[kt][e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
+          if constexpr (C::KT == 1) {
+            pf[kt][e] = p0;
+            pf[kt][e + 1] = p1;
+          } else {
+            le_run += p0 + p1;
+          }
         }
       }
       if constexpr (C::DS == 8) {
-        // per 32-key sub-tile: its K reads, then 8 x (score MFMA + 5 VALU of
-        // the exponentials); sub-tiles one after the other keeps one sub-tile's
-        // K operands live at a time
+        // per 32-key sub-tile: its K reads, then 8 x (score MFMA + the VALU of
+        // the exponentials); sub-tiles one after the other keeps one
+        // sub-tile's K operands live at a time.  With two sub-tiles per step
+        // (64-key tiles) the K reads go four at a time and the fp32 row sum is
+        // taken here: both keep the wave under 256 VGPRs without spills.
+        constexpr int RG = C::KT == 1 ? 8 : 4;  // K reads per group
+        constexpr int VA = C::KT == 1 ? 5 : 7;  // VALU per score MFMA
 #pragma unroll
         for (int kt = 0; kt < C::KT; ++kt) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
 #pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+          for (int g = 0; g < 8 / RG; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x100, RG, 0);
+#pragma unroll
+            for (int i = 0; i < RG; ++i) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x002, VA, 0);
+            }
           }
         }
       }
@@ -542,23 +569,30 @@ void attn_fwd_kernel(AttnArgs a) {
           for (int i = 0; i < 4; ++i)
             l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][4 * half + i]), ones, l_run,
                                                     false);
+          if constexpr (C::KT == 1) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) le_run += pf[kt][8 * half + i];
+          }
         }
       float mx = tile_max(acc_n);
       if constexpr (C::DT == 4) {
         // the first two MFMAs' V reads, then (P V MFMA + the V reads of the
-        // MFMA two ahead + 2 VALU) for all but the last two MFMAs, then 2 x (MFMA
-        // + 2 VALU); the VALU work is the row sums and the max of the next tile
+        // MFMA two ahead + VB VALU) for all but the last two MFMAs, then
+        // 2 x (MFMA + VB VALU); the VALU work is the row sums (with one sub-tile
+        // per step the fp32 one too, here where the VALU is idle rather than
+        // among the exponentials of phase A) and the max of the next tile
+        constexpr int VB = C::KT == 1 ? 4 : 2;
         __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
         for (int i = 0; i < 8 * C::KT - 2; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
         }
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
         }
       }
       if (t + 1 < ntiles) {
@@ -599,12 +633,24 @@ void attn_fwd_kernel(AttnArgs a) {
   }
 
   // ---- write O and lse
-  l_run = half_swap_sum(l_run);  // both lane halves now hold the query's row sum
-  {
-    const float mm = m_run;
-    const float l = l_run;
-    const float inv = l > 0.f ? 1.f / l : 0.f;
-    if (SPLIT && q_ok) {
+  l_run = half_swap_sum(l_run);  // both lane halves now hold the query's row sums
+  le_run = half_swap_sum(le_run);
+  if constexpr (SPLIT) {
+    // Partial result of this key range: the unnormalised P V, scaled by a
+    // power of two 2^-ex per query row so that its largest magnitude lies in
+    // [0.5, 1) and every value keeps fp16's relative precision whatever the
+    // range of V; the merge undoes the scale exactly.
+    float amax = 0.f;
+#pragma unroll
+    for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(acc_o[t][e]));
+    amax = half_swap_max(amax);
+    int ex = 0;
+    if (amax > 0.f && amax <= 3.402823466e38f) ex = __builtin_amdgcn_frexp_expf(amax);
+    ex = ex < -126 ? -126 : ex;
+    const float sc = __builtin_amdgcn_ldexpf(1.0f, -ex);
+    if (q_ok) {
       const int64_t prow = (work * kSplits + split) * BLK + qs * 32 + l32;
       _Float16* po = reinterpret_cast<_Float16*>(a.part_o) + prow * D;
 #pragma unroll
@@ -614,45 +660,43 @@ void attn_fwd_kernel(AttnArgs a) {
           const int d = 32 * t + 8 * g + 4 * hh;
           f16x4 w;
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            w[e] = (_Float16)(acc_o[t][4 * g + e] * inv);
+          for (int e = 0; e < 4; ++e) w[e] = (_Float16)(acc_o[t][4 * g + e] * sc);
           *reinterpret_cast<f16x4*>(po + d) = w;
         }
-      if (hh == 0) {
-        a.part_ml[2 * prow] = mm;
-        a.part_ml[2 * prow + 1] = l;
+      if (hh == 0)
+        reinterpret_cast<float4*>(a.part_meta)[prow] = make_float4(m_run, l_run, le_run, (float)ex);
+    }
+  } else if (q_ok) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    uint16_t* op = a.o + (bh * a.lq + q_row) * D;
+#pragma unroll
+    for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int d = 32 * t + 8 * g + 4 * hh;
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = acc_o[t][4 * g + e] * inv;
+        uint2 w;
+        w.x = pack2_bf16(o[0], o[1]);
+        w.y = pack2_bf16(o[2], o[3]);
+        *reinterpret_cast<uint2*>(op + d) = w;
       }
-    }
-    if (!SPLIT && q_ok) {
-      uint16_t* op = a.o + (bh * a.lq + q_row) * D;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int d = 32 * t + 8 * g + 4 * hh;
-          float o[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            o[e] = acc_o[t][4 * g + e] * inv;
-          uint2 w;
-          w.x = pack2_bf16(o[0], o[1]);
-          w.y = pack2_bf16(o[2], o[3]);
-          *reinterpret_cast<uint2*>(op + d) = w;
-        }
-      if (a.lse != nullptr && hh == 0)
-        a.lse[bh * a.lq + q_row] = l > 0.f ? (mm + log2f(l)) * 0.69314718055994530942f : -INFINITY;
-    }
+    if (a.lse != nullptr && hh == 0)
+      a.lse[bh * a.lq + q_row] = le_run > 0.f ? (m_run + log2f(le_run)) * 0.69314718055994530942f : -INFINITY;
   }
 }
 
-// Combines the kSplits partial results of one query block:
-//   O = sum_r w_r O_r / sum_r w_r,  w_r = l_r 2^(m_r - M),  M = max_r m_r,
-//   lse = ln2 (M + log2 sum_r w_r).
-// Ranges with no visible key (l_r = 0) have weight 0 and their O_r (zeros) add nothing.
+// Combines the kSplits partial results of one query block.  Range r left, per
+// query row, A_r = sum of bf16(p) v over its keys scaled by 2^-e_r (fp16), its
+// running max m_r (log2 units), the row sums lb_r (of the bf16 p that multiply
+// V) and le_r (of the fp32 p), and e_r.  With M = max_r m_r and
+// w_r = 2^(m_r - M) over the ranges that saw a key (lb_r > 0):
+//   O   = sum_r w_r 2^e_r A_r / sum_r w_r lb_r,
+//   lse = ln2 (M + log2 sum_r w_r le_r).
+// Ranges with no visible key have weight 0 and add nothing.
 // One thread per 8-column chunk of the query block's rows (two chunks per
-// thread at BLK = 128, D = 128).  Every thread issues the kSplits partial loads
-// of its first chunk before the weights are computed, so that their latency
-// overlaps that of the (max, sum) pairs.
+// thread at BLK = 128, D = 128).
 template <int D, int BLK>
 struct MergeCfg {
   static constexpr int CPR = D / 8;                     // 8-column chunks per row
@@ -671,13 +715,14 @@ __global__ __launch_bounds__((MergeCfg<D, BLK>::NT)) void attn_merge_kernel(Attn
   const int qb = (int)(work % a.n_q);
   const int tid = threadIdx.x;
   const int64_t rows = a.lq - (int64_t)qb * BLK;
-  // every range's partial is written for every row of the block (zeros when it
-  // saw no key), so the loads need no guard; a zero weight drops the term
+  // every range's partial is written for every real row of the block (zeros
+  // when it saw no key); rows past Lq are never read
   auto load_chunk = [&](int c, f16x8* v) {
     const int row = c / M::CPR, d0 = (c % M::CPR) * 8;
+    const int rr = row < rows ? row : 0;
 #pragma unroll
     for (int r = 0; r < kSplits; ++r) {
-      const int64_t prow = (work * kSplits + r) * BLK + row;
+      const int64_t prow = (work * kSplits + r) * BLK + rr;
       v[r] = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.part_o) + prow * D + d0);
     }
   };
@@ -699,31 +744,39 @@ __global__ __launch_bounds__((MergeCfg<D, BLK>::NT)) void attn_merge_kernel(Attn
     *reinterpret_cast<uint4*>(a.o + (bh * a.lq + (int64_t)qb * BLK + row) * D + d0) = o;
   };
 
+  // The threads of the first BLK rows turn the per-row records into weights
+  // first and then issue their partial loads; every other thread issues its
+  // partial loads at once, so that their latency overlaps the records'.
   f16x8 v[kSplits];
-  load_chunk(tid, v);
-  if (tid < BLK) {
+  if (tid >= BLK) load_chunk(tid, v);
+  if (tid < BLK && tid < rows) {
     const int row = tid;
-    float m[kSplits], l[kSplits], mm = -INFINITY;
+    const float2* rec = reinterpret_cast<const float2*>(a.part_meta);  // record i = float2 pairs 2i, 2i + 1
+    float m[kSplits], lb[kSplits], mm = -INFINITY;
 #pragma unroll
     for (int r = 0; r < kSplits; ++r) {
-      const int64_t prow = (work * kSplits + r) * BLK + row;
-      m[r] = a.part_ml[2 * prow];
-      l[r] = a.part_ml[2 * prow + 1];
-      if (l[r] > 0.f) mm = fmaxf(mm, m[r]);
+      const float2 x = rec[2 * ((work * kSplits + r) * BLK + row)];
+      m[r] = x.x;
+      lb[r] = x.y;
+      if (lb[r] > 0.f) mm = fmaxf(mm, m[r]);
     }
-    float tot = 0.f;
+    float den = 0.f, sum_e = 0.f;
 #pragma unroll
     for (int r = 0; r < kSplits; ++r) {
-      const float w = l[r] > 0.f ? l[r] * exp2f(m[r] - mm) : 0.f;
-      wts[r][row] = w;
-      tot += w;
+      const float2 y = rec[2 * ((work * kSplits + r) * BLK + row) + 1];  // (le, e)
+      const float w = lb[r] > 0.f ? exp2f(m[r] - mm) : 0.f;
+      den = fmaf(w, lb[r], den);
+      sum_e = fmaf(w, y.x, sum_e);
+      wts[r][row] = __builtin_amdgcn_ldexpf(w, (int)y.y);
     }
-    const float inv = tot > 0.f ? 1.f / tot : 0.f;
+    const float inv = den > 0.f ? 1.f / den : 0.f;
 #pragma unroll
     for (int r = 0; r < kSplits; ++r) wts[r][row] *= inv;
-    if (row < rows && a.lse != nullptr)
-      a.lse[bh * a.lq + (int64_t)qb * BLK + row] = tot > 0.f ? (mm + log2f(tot)) * 0.69314718055994530942f : -INFINITY;
+    if (a.lse != nullptr)
+      a.lse[bh * a.lq + (int64_t)qb * BLK + row] =
+          sum_e > 0.f ? (mm + log2f(sum_e)) * 0.69314718055994530942f : -INFINITY;
   }
+  if (tid < BLK) load_chunk(tid, v);
   __syncthreads();
   combine(tid, v);
 #pragma unroll
@@ -754,8 +807,7 @@ static hipError_t launch_cfg(const AttnArgs& a, bool dense, hipStream_t stream) 
 size_t attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block) {
   if (n_k < kSplits) return 0;  // fewer key blocks than ranges: single pass
   const int64_t rows = bh * n_q * kSplits * block;
-  const size_t o_bytes = (size_t(rows * d) * 2 + 255) & ~size_t(255);
-  return o_bytes + size_t(rows) * 2 * sizeof(float);
+  return attn_partial_o_bytes(rows, d) + size_t(rows) * 4 * sizeof(float);
 }
 
 hipError_t launch_attn(const AttnArgs& a, int d, int block, bool dense, hipStream_t stream) {

@@ -336,7 +336,7 @@ static int attn_common(const void* q, const void* k, const void* v, int B, int H
     const int64_t rows = int64_t(B) * H * nq * kSplits * block_size;
     char* ws = static_cast<char*>(workspace);
     a.part_o = reinterpret_cast<uint16_t*>(ws);
-    a.part_ml = reinterpret_cast<float*>(ws + ((size_t(rows * D) * 2 + 255) & ~size_t(255)));
+    a.part_meta = reinterpret_cast<float*>(ws + attn_partial_o_bytes(rows, D));
   }
   hipError_t e = launch_attn(a, D, block_size, dense, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "attention launch: %s", hipGetErrorString(e));

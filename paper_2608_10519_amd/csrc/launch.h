@@ -82,13 +82,18 @@ struct AttnArgs {
   // Key-range split: with part_o set, work item (bh, query block, r) covers key
   // blocks [r n_k / kSplits, (r + 1) n_k / kSplits) and writes a partial result
   // that a merge kernel combines; otherwise one pass writes O and lse.
-  uint16_t* part_o;   // [BH * n_q, kSplits, BLK, D] fp16 partial O normalised by its own row sum
-  float* part_ml;     // [BH * n_q, kSplits, BLK, 2] (running max in log2 units, row sum)
+  uint16_t* part_o;   // [BH * n_q, kSplits, BLK, D] fp16: the range's unnormalised P V times 2^-e per row
+  float* part_meta;   // [BH * n_q, kSplits, BLK, 4]: running max (log2 units), row sum of the bf16 P,
+                      // row sum of the fp32 p, e (the row's power-of-two scale, as a float)
 };
 
 // Key ranges per query block: kSplits / 8 consecutive ranges per XCD, so that
 // each XCD's 4 MB L2 holds about one range of a head's K/V at a time.
 constexpr int kSplits = 16;
+
+// Bytes of the fp16 partial-O region of the split workspace (256-byte aligned;
+// the per-row records follow it).
+inline size_t attn_partial_o_bytes(int64_t rows, int d) { return (size_t(rows * d) * 2 + 255) & ~size_t(255); }
 
 // Bytes of attention workspace for the key-range split (0 when it is not used).
 size_t attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block);

@@ -146,9 +146,10 @@ def _attn(lib, dense=False, **over):
 
 
 def test_attn_workspace_bytes(lib):
-    # 720p: 24 heads x 1125 query blocks x 16 key ranges x 64 rows: fp16 O [.., 128] + fp32 (max, sum)
+    # 720p: 24 heads x 1125 query blocks x 16 key ranges x 64 rows: fp16 partial P V [.., 128] + four fp32
+    # per row (running max, the two row sums, the row's scale exponent)
     rows = 24 * 1125 * 16 * 64
-    want = (rows * 128 * 2 + 255) // 256 * 256 + rows * 8
+    want = (rows * 128 * 2 + 255) // 256 * 256 + rows * 16
     assert S.sparstar_attn_workspace_bytes(1, 24, 72_000, 144_512, 128, 64) == want
     # fewer than 16 key blocks: no split, no workspace
     assert S.sparstar_attn_workspace_bytes(1, 2, 512, 960, 64, 64) == 0

@@ -4,7 +4,7 @@ Small cases are compared element by element; they span several tiles and a
 ragged tail.  Tolerances (tests/helpers.py): selection exact where the oracle's
 boundary gap exceeds 1e-3 (tie-tolerant otherwise), scores |dS| <= 1e-5(1+|S|),
 pooled blocks |d| <= 1e-5, O max-abs <= 1e-2 plus relative Frobenius <= 1e-2 per
-head, lse max-abs <= 4e-3 (the row sum is over bf16-rounded P).
+head, lse max-abs <= 1e-3.
 """
 from __future__ import annotations
 
@@ -277,6 +277,7 @@ def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_ove
     if q_override is not None:
         qb_ = q_override(qb_)
     n_q = -(-w.lq // w.block)
+    _assert_splits(gpu_lib, w, split)
     num, idx = lists_to_device([lists_h], n_q)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
     o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, softmax_scale=scale or 0.0, split=split)
@@ -289,13 +290,23 @@ def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_ove
     return og, lg, o_ref, l_ref, (qb_, kb_, vb_)
 
 
+# Every case has at least 16 key blocks (the number of key ranges of the split
+# path) and a partial last key block, so the split runs for each of the four
+# (D, b) instances; _attn_case asserts that it does.
 ATTN_CASES = [
     ("tiny", TINY),
-    ("d128-b64-ragged", TINY.with_(name="a1", head_dim=128, lq=500, l_ref=300, l_text=77, heads=3, seed=17)),
-    ("d64-b128-ragged", TINY.with_(name="a2", block=128, lq=700, l_ref=515, l_text=130, seed=18)),
+    ("d128-b64-ragged", TINY.with_(name="a1", head_dim=128, lq=500, l_ref=600, l_text=77, heads=3, seed=17)),
+    ("d64-b128-ragged", TINY.with_(name="a2", block=128, lq=700, l_ref=1300, l_text=130, seed=18)),
     ("d128-b128-ragged", TINY.with_(name="a3", head_dim=128, block=128, lq=1000, l_ref=1300, l_text=300,
                                     heads=2, seed=19)),
 ]
+
+
+def _assert_splits(lib, w: Workload, split: bool):
+    """The split path only runs when the library asks for a workspace."""
+    if split:
+        n = lib.sparstar_attn_workspace_bytes(w.batch, w.heads, w.lq, w.lk, w.head_dim, w.block)
+        assert n > 0, f"{w.name}: split requested but the library asks for no workspace"
 
 
 def _random_lists(w: Workload, rng, heads=None):
@@ -374,6 +385,7 @@ def test_dense_attention_matches_oracle(gpu_lib, name, w, split):
     import torch
 
     _say(f"[dense] {name} split={split}")
+    _assert_splits(gpu_lib, w, split)
     qb_, kb_, vb_ = generate(w)
     o, lse = gpu_lib.sparstar_dense_attn_fwd(to_dev(qb_), to_dev(kb_), to_dev(vb_), w.block, split=split)
     torch.cuda.synchronize()
@@ -390,6 +402,7 @@ def test_full_lists_equal_dense(gpu_lib, split):
 
     w = ATTN_CASES[1][1]
     _say(f"[dense==sparse(all)] split={split}")
+    _assert_splits(gpu_lib, w, split)
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
     n_q, n_k = -(-w.lq // w.block), -(-w.lk // w.block)
@@ -525,3 +538,104 @@ def test_empty_query_sequence_is_noop(gpu_lib):
     o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
     torch.cuda.synchronize()
     assert o.numel() == 0 and num.numel() == 0
+
+
+@pytest.mark.parametrize("e", [20, -20, 60, -60])
+@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
+def test_value_magnitudes_far_outside_fp16(gpu_lib, e, split):
+    """V scaled by 2^e (exact in bf16): Eq. 7 is linear in V, so O must scale by
+    exactly 2^e and lse not at all, on the split path (fp16 partials with a
+    per-row power-of-two scale) as on the single pass, and match the oracle.
+    |V| reaches about 5 * 2^60 here, far beyond fp16's 65504, and 2^-60 is far
+    below its smallest normal."""
+    w = ATTN_CASES[1][1]
+    _say(f"[V x 2^{e}] split={split}")
+    lists_h = _random_lists(w, np.random.default_rng(11))
+    og0, lg0, _, _, _ = _attn_case(gpu_lib, w, lists_h, split=split)
+    og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, split=split, v_override=lambda v: _times_pow2(v, e))
+    assert np.array_equal(og, og0 * 2.0 ** e), "O does not scale exactly with V"
+    assert np.array_equal(lg, lg0), "lse depends on the scale of V"
+    check_output(og * 2.0 ** -e, o_ref * 2.0 ** -e, lg, l_ref, what=f"V x 2^{e}")
+
+
+_CANARY = 0x5A  # byte pattern of untouched guard memory
+
+
+def _guarded(shape, dtype, guard=4096):
+    """A contiguous tensor of `shape` inside a canary-filled byte buffer with
+    `guard` bytes before and after it; returns (buffer, view, bytes of the view)."""
+    import torch
+
+    n = int(np.prod(shape)) * torch.empty((), dtype=dtype).element_size()
+    buf = torch.full((guard + n + guard,), _CANARY, dtype=torch.uint8, device="cuda")
+    return buf, buf[guard: guard + n].view(dtype).view(*shape), n
+
+
+def _guards_intact(buf, n, guard=4096):
+    b = buf.cpu().numpy()
+    return bool((b[:guard] == _CANARY).all() and (b[guard + n:] == _CANARY).all())
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_selector_writes_only_its_list_entries(gpu_lib, fused):
+    """kv_indices entries past each row's count are left untouched (the header's
+    promise), with per-head budgets so that the counts differ between heads and a
+    stride wider than needed; nothing outside the two outputs is written."""
+    import torch
+
+    w = ATTN_CASES[1][1]
+    _say(f"[guard] selector fused={fused}")
+    qb_, kb_, _ = generate(w)
+    keep = keep_ranges(w)
+    budgets = [0.1, 0.3, 0.6]
+    n_q = -(-w.lq // w.block)
+    stride = gpu_lib.sparstar_kv_stride(w.heads, w.lk, w.block, budgets, keep) + 5
+    nbuf, num, nn = _guarded((1, w.heads, n_q), torch.int32)
+    ibuf, idx, ni = _guarded((1, w.heads, n_q, stride), torch.int32)
+    gpu_lib.sparstar_score_blocks(to_dev(qb_), to_dev(kb_), w.block, budgets, keep, kv_stride=stride,
+                                  out=(num, idx), fused=fused)
+    torch.cuda.synchronize()
+    assert _guards_intact(nbuf, nn) and _guards_intact(ibuf, ni), "a write outside the outputs"
+    canary = np.frombuffer(bytes([_CANARY] * 4), dtype=np.int32)[0]
+    n, ix = num.cpu().numpy(), idx.cpu().numpy()
+    keep_set = O.keep_blocks(keep, w.lk, w.block)
+    n_sel = -(-w.lk // w.block) - len(keep_set)
+    for h, rho in enumerate(budgets):
+        c = len(keep_set) + O.budget_k(rho, n_sel)
+        assert (n[0, h] == c).all()
+        assert (ix[0, h, :, c:] == canary).all(), f"head {h}: an entry past the count was written"
+        assert (ix[0, h, :, :c] != canary).all()
+
+
+@pytest.mark.parametrize("dense", [False, True], ids=["sparse", "dense"])
+@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
+def test_attention_writes_only_its_outputs(gpu_lib, dense, split):
+    """O and lse sit inside canary-filled guard bands; the last query block is
+    partial (Lq = 500 at b = 64), so rows past Lq would land in the band after
+    the last head.  Nothing outside O and lse changes, and the result matches
+    the oracle."""
+    import torch
+
+    w = ATTN_CASES[1][1]
+    _say(f"[guard] attention dense={dense} split={split}")
+    _assert_splits(gpu_lib, w, split)
+    qb_, kb_, vb_ = generate(w)
+    q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
+    n_q = -(-w.lq // w.block)
+    assert w.lq % w.block != 0
+    lists_h = _random_lists(w, np.random.default_rng(5))
+    obuf, o, no = _guarded((1, w.heads, w.lq, w.head_dim), torch.bfloat16)
+    lbuf, lse, nl = _guarded((1, w.heads, w.lq), torch.float32)
+    if dense:
+        gpu_lib.sparstar_dense_attn_fwd(q, k, v, w.block, out=o, lse=lse, split=split)
+        lists_h = [[list(range(-(-w.lk // w.block)))] * n_q for _ in range(w.heads)]
+    else:
+        num, idx = lists_to_device([lists_h], n_q)
+        gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, out=o, lse=lse, split=split)
+    torch.cuda.synchronize()
+    assert _guards_intact(obuf, no), "O: a write outside the output"
+    assert _guards_intact(lbuf, nl), "lse: a write outside the output"
+    refs = [O.sparse_attention(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), bf16_to_f64(vb_[0, h]),
+                               lists_h[h], w.block) for h in range(w.heads)]
+    check_output(bf16_tensor_to_f64(o), np.stack([r[0] for r in refs])[None], lse.cpu().numpy().astype(np.float64),
+                 np.stack([r[1] for r in refs])[None], what="guarded")
