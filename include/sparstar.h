@@ -117,6 +117,34 @@ int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq
                           int n_keep, int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride, float* scores,
                           void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of device scratch the library holds per GPU for sparstar_score_blocks_static (64 MiB). */
+#define SPARSTAR_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/*
+ * sparstar_score_blocks for callers that cannot allocate device memory, not
+ * even a workspace: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  Same arguments, results and errors as
+ * sparstar_score_blocks, without the workspace: its scratch (the pooled blocks
+ * qbar and kbar, and S when `scores` is NULL) lives in a device array of
+ * SPARSTAR_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends.  With `scores` given, S goes there and only
+ * qbar + kbar use the scratch (41.6 MB at 24 heads, 72,000 queries and
+ * 144,512 keys in 64-token blocks); sizes that need more than the scratch
+ * return SPARSTAR_ERR_WORKSPACE before any HIP call.
+ *   - The call allocates nothing: no hipMalloc, hipFree or allocating library
+ *     routine.  The first call on a device looks up the array's device address
+ *     there (hipGetSymbolAddress) and keeps it.
+ *   - Every call on one GPU shares that GPU's array, which keeps the contents
+ *     of the last call; nothing in it needs to start at zero.  Calls that
+ *     overlap on one GPU (concurrent streams, or host threads) race on it: the
+ *     caller must order them.
+ *   - Devices 0..63 are served; others return SPARSTAR_ERR_UNSUPPORTED.
+ */
+int sparstar_score_blocks_static(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
+                                 int block_size, const double* budget, int n_budget, const sparstar_range* keep,
+                                 int n_keep, int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride,
+                                 float* scores, void* stream);
+
 /* Most key blocks per row that sparstar_score_blocks_fused accepts. */
 #define SPARSTAR_FUSED_MAX_BLOCKS 2304
 

@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libsparstar.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["host_api.cpp", "pool_score.hip", "select.hip", "attn_fwd.hip", "mass.hip"]
+SOURCES = ["host_api.cpp", "pool_score.hip", "select.hip", "attn_fwd.hip", "mass.hip", "static_scratch.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "../../include/sparstar.h"
+#include "host_internal.h"
 #include "launch.h"
 
 namespace {
@@ -201,10 +202,14 @@ extern "C" size_t sparstar_score_workspace_bytes(int B, int H, int64_t Lq, int64
   return ws_layout(B, H, Lq, Lk, D, block_size).total;
 }
 
+// s_outside: S may live in the caller's `scores` output instead of the
+// workspace, which then only needs the pooled blocks.  validate_only: check
+// every argument (the workspace by its size only) and launch nothing.
 static int score_common(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D, int block_size,
                         const double* budget, int n_budget, const sparstar_range* keep, int n_keep,
                         int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride, float* scores, void* workspace,
-                        size_t workspace_bytes, void* stream, bool fused) {
+                        size_t workspace_bytes, void* stream, bool fused, bool s_outside = false,
+                        bool validate_only = false) {
   using namespace sparstar;
   if (int rc = check_sizes(B, H, Lq, Lk, D, block_size)) return rc;
   // With Lq == 0 there is nothing to read or write on the query side.
@@ -223,17 +228,20 @@ static int score_common(const void* q, const void* k, int B, int H, int64_t Lq, 
     return fail(SPARSTAR_ERR_INVALID_ARG, "kv_stride %d < |J_keep| + max k = %lld", kv_stride,
                 (long long)(n_keep_blocks + max_k));
   const WsLayout wl = ws_layout(B, H, Lq, Lk, D, block_size);
-  if (!workspace) return fail(SPARSTAR_ERR_WORKSPACE, "workspace is null");
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-    return fail(SPARSTAR_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-  if (workspace_bytes < wl.total)
-    return fail(SPARSTAR_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, wl.total);
+  const size_t need = (s_outside && scores) ? wl.s : wl.total;
+  if (!validate_only) {
+    if (!workspace) return fail(SPARSTAR_ERR_WORKSPACE, "workspace is null");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+      return fail(SPARSTAR_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  }
+  if (workspace_bytes < need)
+    return fail(SPARSTAR_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
   if (scores && (reinterpret_cast<uintptr_t>(scores) & 3u) != 0)
     return fail(SPARSTAR_ERR_INVALID_ARG, "scores must be 4-byte aligned");
   if (fused && nk > kFusedMaxBlocks)
     return fail(SPARSTAR_ERR_UNSUPPORTED, "fused scores and selection take at most %d key blocks (got %lld)",
                 kFusedMaxBlocks, (long long)nk);
-  if (nq == 0) return ok();
+  if (nq == 0 || validate_only) return ok();
 
   const int bh = B * H;
   char* ws = static_cast<char*>(workspace);
@@ -272,6 +280,25 @@ extern "C" int sparstar_score_blocks(const void* q, const void* k, int B, int H,
   return score_common(q, k, B, H, Lq, Lk, D, block_size, budget, n_budget, keep, n_keep, kv_num_blocks, kv_indices,
                       kv_stride, scores, workspace, workspace_bytes, stream, false);
 }
+
+namespace sparstar {
+
+int score_blocks_internal(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D, int block_size,
+                          const double* budget, int n_budget, const sparstar_range* keep, int n_keep,
+                          int32_t* kv_num_blocks, int32_t* kv_indices, int kv_stride, float* scores, void* workspace,
+                          size_t workspace_bytes, void* stream, bool validate_only) {
+  return score_common(q, k, B, H, Lq, Lk, D, block_size, budget, n_budget, keep, n_keep, kv_num_blocks, kv_indices,
+                      kv_stride, scores, workspace, workspace_bytes, stream, false, true, validate_only);
+}
+
+int report_error(int code, const char* msg) { return fail(code, "%s", msg); }
+
+size_t score_pooled_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
+  if (check_sizes(B, H, Lq, Lk, D, block_size) != SPARSTAR_OK) return 0;
+  return ws_layout(B, H, Lq, Lk, D, block_size).s;
+}
+
+}  // namespace sparstar
 
 extern "C" int sparstar_score_blocks_fused(const void* q, const void* k, int B, int H, int64_t Lq, int64_t Lk, int D,
                                            int block_size, const double* budget, int n_budget,

@@ -20,6 +20,7 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 MAX_KEEP_RANGES = 8
 FUSED_MAX_BLOCKS = 2304  # SPARSTAR_FUSED_MAX_BLOCKS
 MAX_MASS_ROWS = 16
+STATIC_SCRATCH_BYTES = 64 << 20  # SPARSTAR_STATIC_SCRATCH_BYTES
 
 _lib = None
 
@@ -56,6 +57,9 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.sparstar_score_blocks_fused.argtypes = [c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_dp, c_i, c_rp, c_i,
                                                 c_p, c_p, c_i, c_p, c_sz, c_p]
     lib.sparstar_score_blocks_fused.restype = c_i
+    lib.sparstar_score_blocks_static.argtypes = [c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_dp, c_i, c_rp, c_i,
+                                                 c_p, c_p, c_i, c_p, c_p]
+    lib.sparstar_score_blocks_static.restype = c_i
     lib.sparstar_attn_workspace_bytes.argtypes = [c_i, c_i, c_i64, c_i64, c_i, c_i]
     lib.sparstar_attn_workspace_bytes.restype = c_sz
     lib.sparstar_sparse_attn_fwd.argtypes = [c_p, c_p, c_p, c_i, c_i, c_i64, c_i64, c_i, c_i, c_p, c_p, c_i,
@@ -205,6 +209,33 @@ def sparstar_score_blocks(q: torch.Tensor, k: torch.Tensor, block_size: int, bud
                                        scores.data_ptr() if scores is not None else None,
                                        workspace.data_ptr(), ws_n, _stream())
         _check("sparstar_score_blocks", rc)
+    return num, idx
+
+
+def sparstar_score_blocks_static(q: torch.Tensor, k: torch.Tensor, block_size: int, budget, keep=(), *,
+                                 kv_stride: int | None = None, scores: torch.Tensor | None = None, out=None):
+    """The selector with its scratch in the library's static per-GPU buffer
+    (sparstar_score_blocks_static): the C call allocates nothing.  Pass `out`
+    (and `scores` where S does not fit the scratch) to allocate nothing here
+    either.  Returns (kv_num_blocks, kv_indices)."""
+    B, H, Lq, D = _bhld(q, "q")
+    Bk, Hk, Lk, Dk = _bhld(k, "k")
+    if (B, H, D) != (Bk, Hk, Dk):
+        raise ValueError("q and k disagree on B, H or D")
+    bud, nb = _budget_array(budget)
+    kr, nkeep = _keep_array(keep)
+    if kv_stride is None:
+        kv_stride = sparstar_kv_stride(H, Lk, block_size, budget, keep)
+    n_q = -(-Lq // block_size)
+    if out is None:
+        num = torch.empty((B, H, n_q), dtype=torch.int32, device=q.device)
+        idx = torch.empty((B, H, n_q, kv_stride), dtype=torch.int32, device=q.device)
+    else:
+        num, idx = out
+    rc = load().sparstar_score_blocks_static(q.data_ptr(), k.data_ptr(), B, H, Lq, Lk, D, block_size, bud, nb, kr,
+                                             nkeep, num.data_ptr(), idx.data_ptr(), kv_stride,
+                                             scores.data_ptr() if scores is not None else None, _stream())
+    _check("sparstar_score_blocks_static", rc)
     return num, idx
 
 

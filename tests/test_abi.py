@@ -128,6 +128,48 @@ def test_score_blocks_fused_rejects_invalid_arguments(lib, over, code, msg):
     assert msg in S.last_error()
 
 
+def _score_static(lib, **over):
+    a = dict(q=FAKE, k=FAKE, B=1, H=2, Lq=512, Lk=1152, D=64, block=64, budget=[0.25], keep=[(0, 128)], num=FAKE,
+             idx=FAKE, stride=6, scores=None)
+    a.update(over)
+    bud = (ctypes.c_double * len(a["budget"]))(*a["budget"]) if a["budget"] is not None else None
+    kr = (S.Range * max(1, len(a["keep"])))(*[S.Range(x, y) for x, y in a["keep"]])
+    return lib.sparstar_score_blocks_static(a["q"], a["k"], a["B"], a["H"], a["Lq"], a["Lk"], a["D"], a["block"],
+                                            bud, len(a["budget"]) if a["budget"] is not None else 1, kr,
+                                            a.get("n_keep", len(a["keep"])), a["num"], a["idx"], a["stride"],
+                                            a["scores"], None)
+
+
+@pytest.mark.parametrize("over,code,msg", [
+    (dict(D=96), S.ERR_UNSUPPORTED, "head dim"),
+    (dict(q=FAKE + 2), S.ERR_INVALID_ARG, "16-byte"),
+    (dict(budget=[1.5]), S.ERR_INVALID_ARG, "outside [0, 1]"),
+    (dict(keep=[(0, 2000)]), S.ERR_INVALID_ARG, "keep[0]"),
+    (dict(stride=5), S.ERR_INVALID_ARG, "kv_stride"),
+    (dict(scores=FAKE + 2), S.ERR_INVALID_ARG, "scores"),
+    # the 720p shape (24 heads, 72,000 queries, 144,512 keys, D 128): qbar + kbar + S = 285 MB
+    (dict(H=24, Lq=72_000, Lk=144_512, D=128, keep=[(72_000, 72_512)], stride=571), S.ERR_WORKSPACE,
+     "more than the 67108864 bytes"),
+])
+def test_score_blocks_static_rejects_before_any_hip_call(lib, over, code, msg):
+    """Every argument, the static scratch's size included, is checked on the host
+    first: without a GPU these calls return their own error, never a HIP one."""
+    assert _score_static(lib, **over) == code
+    assert msg in S.last_error()
+
+
+def test_score_blocks_static_scratch_limit():
+    """With `scores` given, S stays out of the static scratch: at the 720p shape
+    qbar + kbar (41.6 MB) fit, which the next check (a too-small stride) shows."""
+    lib = S.load()
+    big = dict(H=24, Lq=72_000, Lk=144_512, D=128, keep=[(72_000, 72_512)])
+    assert _score_static(lib, **big, stride=5, scores=FAKE) == S.ERR_INVALID_ARG
+    assert "kv_stride" in S.last_error()
+    assert _score_static(lib, **big, stride=571) == S.ERR_WORKSPACE
+    # an empty query side is a no-op that makes no HIP call
+    assert _score_static(lib, Lq=0) == S.OK and S.last_error() == ""
+
+
 def test_score_blocks_fused_takes_the_limit_on_an_empty_query_side(lib):
     # Lq = 0 is a no-op that touches no device memory, after the size checks
     assert _score_fused(lib, Lq=0, Lk=64 * S.FUSED_MAX_BLOCKS, stride=1000) == S.OK
