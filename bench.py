@@ -86,42 +86,63 @@ def _cpu_model() -> str:
     return platform.processor() or platform.machine()
 
 
-def cpu_baseline(w, qb, kb, vb, keep, total_flops: float, lists_gpu) -> dict:
-    """Time the oracle on head 0: the whole selector for that head, plus the
-    attention of a sample of query blocks; scale to all heads and blocks."""
+CPU_SELECTOR_HEADS = (0, 12)   # heads whose whole selector the oracle runs
+CPU_ATTN_BLOCKS = 480           # (head, query block) pairs of the forward, spread over heads and blocks
+
+
+def cpu_baseline(w, qb, kb, vb, keep_ref, total_flops: float, idx_gpu, num_gpu) -> dict:
+    """The float64 oracle, as it stands, on a bounded sample of the headline
+    workload: the whole selector of CPU_SELECTOR_HEADS, and the forward of
+    CPU_ATTN_BLOCKS (head, query block) pairs spread over all heads and blocks.
+    The per-head selector time and the per-block forward time are scaled to the
+    whole call (24 heads x 1,125 blocks); the value is therefore extrapolated."""
     import oracle as O
     from synthetic import bf16_to_f64
 
+    cores = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)
     except Exception:  # pragma: no cover
-        threads = 1
-    n_q = w.lq // w.block
-    q = bf16_to_f64(qb[0, 0])
-    k = bf16_to_f64(kb[0, 0])
-    v = bf16_to_f64(vb[0, 0])
-    t0 = time.perf_counter()
-    lists, _, _, _ = O.select(q, k, w.block, w.density, keep)
-    t_sel = time.perf_counter() - t0
-    sample = sorted(set(np.linspace(0, n_q - 1, 48).astype(int).tolist()))
-    t0 = time.perf_counter()
-    for i in sample:
-        rows = slice(i * w.block, (i + 1) * w.block)
-        O.sparse_attention(q[rows], k, v, [lists[i]], w.block)
-    t_att = (time.perf_counter() - t0) / len(sample)
-    est_s = w.heads * (t_sel + n_q * t_att)
-    agree = sum(int(lists[i] == lists_gpu[i]) for i in range(n_q)) / n_q
+        limiter = None
+    n_q = -(-w.lq // w.block)
+    t_sel, agree = [], []
+    for h in CPU_SELECTOR_HEADS:
+        q, k = bf16_to_f64(qb[0, h]), bf16_to_f64(kb[0, h])
+        t0 = time.perf_counter()
+        lists, _, _, _ = O.select(q, k, w.block, w.density, keep_ref)
+        t_sel.append(time.perf_counter() - t0)
+        agree.append(sum(int(lists[i] == idx_gpu[0, h, i, : num_gpu[0, h, i]].tolist()) for i in range(n_q)) / n_q)
+    rng = np.random.default_rng(7)
+    pairs = sorted((int(h), int(i)) for h, i in zip(rng.integers(0, w.heads, CPU_ATTN_BLOCKS),
+                                                      np.linspace(0, n_q - 1, CPU_ATTN_BLOCKS).astype(int)))
+    t_att = 0.0
+    cur, kv = None, None
+    for h, i in pairs:
+        if cur != h:
+            cur, kv = h, (bf16_to_f64(qb[0, h]), bf16_to_f64(kb[0, h]), bf16_to_f64(vb[0, h]))
+        q, k, v = kv
+        rows = slice(i * w.block, min((i + 1) * w.block, w.lq))
+        t0 = time.perf_counter()
+        O.sparse_attention(q[rows], k, v, [idx_gpu[0, h, i, : num_gpu[0, h, i]].tolist()], w.block)
+        t_att += time.perf_counter() - t0
+    if limiter is not None:
+        limiter.unregister()
+    per_sel, per_blk = float(np.mean(t_sel)), t_att / len(pairs)
+    est_s = w.heads * (per_sel + n_q * per_blk)
     return {
         "value": total_flops / est_s / 1e12,
         "unit": "TFLOP/s",
         "ms_per_call": est_s * 1e3,
-        "cores": int(threads),
+        "cores": cores,
         "kind": "oracle",
-        "sample": (f"head 0 of 24: full selector ({n_q} rows, {t_sel:.1f} s) + attention of {len(sample)} "
-                   f"evenly spaced query blocks ({t_att:.3f} s each), scaled to 24 heads x {n_q} blocks"),
+        "method": "extrapolated",
+        "sample": (f"extrapolated from a sample: the full selector of heads {list(CPU_SELECTOR_HEADS)} "
+                   f"({n_q} rows each, {per_sel:.2f} s per head) and the forward of {len(pairs)} (head, query "
+                   f"block) pairs spread over all heads and blocks ({per_blk * 1e3:.1f} ms each, on the GPU's "
+                   f"lists), scaled to {w.heads} heads x {n_q} blocks; {sum(t_sel) + t_att:.1f} s of CPU work"),
         "cpu": _cpu_model(),
-        "lists_equal_gpu_head0": agree,
+        "lists_equal_gpu_sampled_heads": float(np.mean(agree)),
     }
 
 
@@ -133,9 +154,8 @@ class Runner:
         dev = torch.device("cuda:0")
         up = lambda bits: torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
         self.q, self.k, self.v = up(qb), up(kb), up(vb)
-        from synthetic import keep_ranges
-
-        self.keep = keep_ranges(w)
+        seg = w.segments()
+        self.keep = S.sparstar_clip_keep_ranges(2, seg["text"], seg["ref"])  # Eq. 3: later clips keep the text
         self.budget = budget
         B, H, Lq, D = self.q.shape
         Lk = self.k.shape[2]
@@ -235,6 +255,14 @@ def attention_mass(r: "Runner", S, torch) -> dict:
             "data": "synthetic (no trained model): absolute values are not the paper's"}
 
 
+def _stats(xs) -> dict:
+    return {"mean": float(np.mean(xs)), "median": float(np.median(xs)), "min": float(np.min(xs)),
+            "p90": float(np.percentile(xs, 90))}
+
+
+FLUSH_BYTES = 512 << 20  # larger than the L2s (8 x 4 MB) and the 256 MB last-level cache together
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -244,13 +272,15 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
-    ap.add_argument("--no-pyramid", action="store_true")
-    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache selector timing")
+    ap.add_argument("--no-pyramid", action="store_true", help="skip both pyramid legs")
+    ap.add_argument("--no-mid", action="store_true", help="skip the mid-scale leg")
+    ap.add_argument("--no-warm", action="store_true", help="skip the warm-cache step timing")
     ap.add_argument("--no-b128", action="store_true", help="skip the 720p run at block size 128")
     ap.add_argument("--no-mass", action="store_true", help="skip the retained-attention-mass diagnostic")
     ap.add_argument("--no-graph", action="store_true", help="skip the graph-captured step timing")
     ap.add_argument("--gen-workers", type=int, default=None,
-                    help="input-generation processes (1 = in-process; use 1 under a profiler)")
+                    help="input-generation processes (default: up to 16; generation runs in-process "
+                         "under a profiler regardless)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB -> 1 GiB fp32 copy kernel 3 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -271,18 +301,19 @@ def main() -> int:
         print(json.dumps({"copy_calibration": {"read_bytes": 4 * n, "write_bytes": 4 * n, "launches": 3}}))
         return 0
 
-    from synthetic import P720, SWEEP, SWEEP_DENSITIES, generate, head_densities, pyramid_scales
+    from synthetic import MID, P720, SWEEP, SWEEP_DENSITIES, generate, head_densities, pyramid_scales
 
     # all inputs are generated before the GPU is touched
     w = P720 if args.density is None else P720.with_(density=args.density)
     log(f"generating {w.name}: H={w.heads} D={w.head_dim} b={w.block} Lq={w.lq} Lk={w.lk} rho={w.density}")
     t0 = time.perf_counter()
-    data = generate(w, workers=args.gen_workers)
+    gw = args.gen_workers
+    data = generate(w, workers=gw)
     w128 = w.with_(name="720p-b128", block=128)
-    b128_data = None if args.no_b128 else generate(w128, workers=args.gen_workers)
-    sweep_data = None if args.no_sweep else generate(SWEEP, workers=args.gen_workers)
-    pyr = [] if args.no_pyramid else [(pw, sparse, generate(pw, workers=args.gen_workers))
-                                      for pw, sparse in pyramid_scales()]
+    b128_data = None if args.no_b128 else generate(w128, workers=gw)
+    sweep_data = None if args.no_sweep else generate(SWEEP, workers=gw)
+    mid_data = None if args.no_mid else generate(MID, workers=gw)
+    pyr = [] if args.no_pyramid else [(pw, sparse, generate(pw, workers=gw)) for pw, sparse in pyramid_scales()]
     log(f"generated in {time.perf_counter() - t0:.1f} s")
 
     import torch
@@ -292,6 +323,10 @@ def main() -> int:
     S.load()
     r = Runner(S, torch, w, *data, w.density)
     B, H, Lq, Lk, D = r.shape
+    flush_buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda:0")
+
+    def flush():
+        flush_buf.fill_(1)
 
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -299,11 +334,15 @@ def main() -> int:
         r.sparse()
     torch.cuda.synchronize()
 
-    log(f"timing {args.steps} steps")
+    # The timed region: K steps, each after a 512 MiB write that evicts the L2s
+    # and the last-level cache (cold caches, as the measurement protocol asks),
+    # with HIP events around the selector call and the sparse forward call.
+    log(f"timing {args.steps} steps (512 MiB cache flush before each)")
     marks = [(r.ev(), r.ev(), r.ev()) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for m in marks:
+        flush()
         m[0].record()
         r.score()
         m[1].record()
@@ -313,14 +352,15 @@ def main() -> int:
     wall = time.perf_counter() - t0
     sel_ms = [m[0].elapsed_time(m[1]) for m in marks]
     att_ms = [m[1].elapsed_time(m[2]) for m in marks]
-    ms_step = wall * 1e3 / args.steps
+    step_ms = [a + b for a, b in zip(sel_ms, att_ms)]
+    ms_step = float(np.median(step_ms))
 
     counts = r.num.cpu().numpy()
     flops = r.flops()
     att_avg = float(np.mean(att_ms))
     achieved = flops / (att_avg * 1e-3) / 1e12
-    log(f"step {ms_step:.3f} ms  selector {np.mean(sel_ms):.3f} ms  sparse fwd {att_avg:.3f} ms  "
-        f"({achieved:.1f} TFLOP/s)")
+    log(f"step median {ms_step:.3f} ms (min {np.min(step_ms):.3f}, p90 {np.percentile(step_ms, 90):.3f})  "
+        f"selector {np.median(sel_ms):.3f} ms  sparse fwd {np.median(att_ms):.3f} ms ({achieved:.1f} TFLOP/s)")
     tr = traffic_from_profile()
 
     out = {
@@ -343,15 +383,17 @@ def main() -> int:
             "kv_blocks_per_row": int(counts.max()),
             "executed_tflop": flops / 1e12,
         },
+        "timing": {
+            "protocol": "HIP events around each call; a 512 MiB write before each of the K timed steps "
+                        "(cold L2 and last-level cache); ms_per_step is the median step",
+            "step_ms": _stats(step_ms),
+            "wall_ms_per_step_incl_flush": wall * 1e3 / args.steps,
+        },
         "breakdown_ms": {
-            "score_blocks": float(np.mean(sel_ms)),
-            "score_blocks_median": float(np.median(sel_ms)),
-            "score_blocks_min": float(np.min(sel_ms)),
-            "score_blocks_p90": float(np.percentile(sel_ms, 90)),
-            "sparse_attn_fwd": att_avg,
-            "sparse_attn_fwd_median": float(np.median(att_ms)),
-            "sparse_attn_fwd_min": float(np.min(att_ms)),
-            "sparse_attn_fwd_p90": float(np.percentile(att_ms, 90)),
+            "score_blocks": float(np.median(sel_ms)),
+            "score_blocks_stats": _stats(sel_ms),
+            "sparse_attn_fwd": float(np.median(att_ms)),
+            "sparse_attn_fwd_stats": _stats(att_ms),
         },
         "roofline": {
             "bound": "mfma",
@@ -365,26 +407,24 @@ def main() -> int:
     }
     if tr is not None:
         out["roofline"]["traffic_detail_bytes"] = tr
+    read_bytes = 2.0 * B * H * (Lq + Lk) * D  # Q and K, bf16, read once by the pooling kernel
+    out["breakdown_ms"]["score_blocks_hbm_TBps"] = read_bytes / (np.median(sel_ms) * 1e-3) / 1e12
 
-    if not args.no_cold:
-        # the selector from cold caches: a 512 MiB write evicts L2 and MALL
-        # before each rep, so Q and K come from HBM
-        scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
-        cold = []
-        for _ in range(5):
-            scratch.fill_(1)
-            a, b = r.ev(), r.ev()
-            a.record()
+    if not args.no_warm:
+        # the same step with warm caches (no flush), for comparison
+        wm = [(r.ev(), r.ev(), r.ev()) for _ in range(args.steps)]
+        for m in wm:
+            m[0].record()
             r.score()
-            b.record()
-            torch.cuda.synchronize()
-            cold.append(a.elapsed_time(b))
-        del scratch
-        read_bytes = 2.0 * B * H * (Lq + Lk) * D  # Q and K, bf16, read once by the pooling kernel
-        out["breakdown_ms"]["score_blocks_cold_median"] = float(np.median(cold))
-        out["breakdown_ms"]["score_blocks_cold_min"] = float(np.min(cold))
-        log(f"selector from cold caches: median {np.median(cold):.3f} ms "
-            f"({read_bytes / (np.median(cold) * 1e-3) / 1e12:.2f} TB/s of Q+K over the whole selector call)")
+            m[1].record()
+            r.sparse()
+            m[2].record()
+        torch.cuda.synchronize()
+        wsel = [m[0].elapsed_time(m[1]) for m in wm]
+        watt = [m[1].elapsed_time(m[2]) for m in wm]
+        out["timing"]["warm"] = {"step_ms": _stats([a + b for a, b in zip(wsel, watt)]),
+                                 "score_blocks_ms": _stats(wsel), "sparse_attn_fwd_ms": _stats(watt)}
+        log(f"warm: step {np.median(wsel) + np.median(watt):.3f} ms, selector {np.median(wsel):.3f} ms")
 
     n_k = -(-Lk // w.block)
     if n_k <= S.FUSED_MAX_BLOCKS:
@@ -397,9 +437,8 @@ def main() -> int:
                                     out=(fnum, fidx), fused=True)
 
         f_ms = r.timed(fused, reps=10, warm=2)
-        out["breakdown_ms"]["score_blocks_fused"] = float(np.mean(f_ms))
-        out["breakdown_ms"]["score_blocks_fused_median"] = float(np.median(f_ms))
-        log(f"fused score/select selector: {np.mean(f_ms):.3f} ms (separate kernels {np.mean(sel_ms):.3f} ms)")
+        out["breakdown_ms"]["score_blocks_fused"] = float(np.median(f_ms))
+        log(f"fused score/select selector: {np.median(f_ms):.3f} ms (separate kernels {np.median(sel_ms):.3f} ms)")
         del fnum, fidx
 
     if not args.no_graph:
@@ -425,21 +464,21 @@ def main() -> int:
             graph.replay()
         torch.cuda.synchronize()
         g_ms = (time.perf_counter() - t0) * 1e3 / args.steps
-        out["graph"] = {"ms_per_step": g_ms, "speedup_vs_eager": ms_step / g_ms}
-        log(f"graph step {g_ms:.3f} ms (eager {ms_step:.3f} ms)")
+        out["graph"] = {"ms_per_step_warm": g_ms}
+        log(f"graph step {g_ms:.3f} ms (warm)")
         del graph
 
     dense_ms = None
     if not args.no_dense:
         log("dense comparison")
-        dense_ms = float(np.mean(r.timed(r.dense, 2)))
+        dense_ms = float(np.median(r.timed(r.dense, 3)))
         out["dense"] = {
             "ms": dense_ms,
             "tflops": r.dense_flops() / (dense_ms * 1e-3) / 1e12,
             "speedup_sparse_step": dense_ms / ms_step,
-            "speedup_sparse_fwd_only": dense_ms / att_avg,
+            "speedup_sparse_fwd_only": dense_ms / float(np.median(att_ms)),
         }
-        log(f"dense {dense_ms:.2f} ms -> speedup {dense_ms / ms_step:.2f}x (step), {dense_ms / att_avg:.2f}x (fwd)")
+        log(f"dense {dense_ms:.2f} ms -> speedup {dense_ms / ms_step:.2f}x (step)")
 
     if not args.no_mass:
         log("retained attention mass (selection vs token-wise top-K bound)")
@@ -447,6 +486,38 @@ def main() -> int:
         for row in out["attention_mass"]["by_density"]:
             log(f"  rho={row['density']}: block top-k keeps {row['block_mean']:.4f} of the dense mass "
                 f"(sampled rows {row['block_mean_sampled']:.4f}, token bound {row['token_bound_mean_sampled']:.4f})")
+
+    def cold_timed(rr, fn, reps):
+        """Event times of fn, each rep after the cache flush."""
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            flush()
+            a, b = rr.ev(), rr.ev()
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return ts
+
+    if mid_data is not None:
+        log("mid scale (11,520 queries against 84,032 keys)")
+        rm = Runner(S, torch, MID, *mid_data, MID.density)
+        sc = cold_timed(rm, rm.score, 10)
+        sp = cold_timed(rm, rm.sparse, 10)
+        fl = rm.flops()
+        mB, mH, mLq, mLk, mD = rm.shape
+        mbytes = 2.0 * mB * mH * (mLq + mLk) * mD
+        out["mid"] = {"workload": "mid scale: B=1, H=24, D=128, block 64, Lq=11520, Lk=84032 (72000 preceding-"
+                                  "clip + 512 text + 11520 current), text forced, budget 25%",
+                      "score_ms": float(np.median(sc)), "sparse_fwd_ms": float(np.median(sp)),
+                      "executed_tflop": fl / 1e12, "tflops": fl / (np.median(sp) * 1e-3) / 1e12,
+                      "scoring_read_bytes": mbytes, "score_hbm_TBps": mbytes / (np.median(sc) * 1e-3) / 1e12,
+                      "kv_blocks_per_row": int(rm.num.max().item())}
+        log(f"  mid: score {np.median(sc):.3f} ms, sparse {np.median(sp):.3f} ms ({out['mid']['tflops']:.0f} TFLOP/s)")
+        del rm
 
     if b128_data is not None:
         log("720p at the paper's deployed block size 128")
@@ -468,8 +539,8 @@ def main() -> int:
         for rho in SWEEP_DENSITIES:
             budgets = head_densities(SWEEP, rho).tolist()
             rs = Runner(S, torch, SWEEP, *sweep_data, budgets)
-            sc = float(np.mean(rs.timed(rs.score, 3)))
-            sp = float(np.mean(rs.timed(rs.sparse, 3)))
+            sc = float(np.median(rs.timed(rs.score, 5)))
+            sp = float(np.median(rs.timed(rs.sparse, 5)))
             fl = rs.flops()
             row = {"density": rho, "score_ms": sc, "sparse_fwd_ms": sp, "step_ms": sc + sp,
                    "executed_tflop": fl / 1e12, "tflops": fl / (sp * 1e-3) / 1e12,
@@ -483,30 +554,42 @@ def main() -> int:
         out["sweep"] = rows
 
     if pyr:
-        log("clip pyramid (dense scales 1-3, fresh selection + sparse scales 4-5)")
-        scales, total = [], 0.0
-        for pw, sparse, pdata in pyr:
-            rp = Runner(S, torch, pw, *pdata, pw.density)
-            if sparse:
-                ms = float(np.mean(rp.timed(lambda: (rp.score(), rp.sparse()), 2)))
-                fl = rp.flops()
-            else:
-                ms = float(np.mean(rp.timed(rp.dense, 2)))
-                fl = rp.dense_flops()
-            total += ms
-            scales.append({"lq": pw.lq, "lk": pw.lk, "mode": "sparse" if sparse else "dense", "ms": ms,
-                           "executed_tflop": fl / 1e12})
-            log(f"  Lq={pw.lq}: {'sparse' if sparse else 'dense'} {ms:.2f} ms")
-            del rp
-        out["pyramid"] = {"total_ms": total, "scales": scales}
+        # the configured pyramid (dense scales 1-3, fresh selection at 25% on
+        # scales 4-5), then the paper's scale-wise density schedule: the four
+        # finest scales sparsified at (0.625, 0.1875, 0.1875, 0.09375), looked
+        # up by query length (sparstar_scale_densities), the coarsest dense
+        lqs = [pw.lq for pw, _, _ in pyr]
+        sched = S.sparstar_scale_densities(lqs, S.PAPER_720P_FINEST_DENSITIES)
+        for leg, modes in (("pyramid", [(0.25 if sp_ else None) for _, sp_, _ in pyr]),
+                           ("pyramid_paper_schedule", sched)):
+            log(f"clip pyramid: {leg}")
+            scales, total, dense_total = [], 0.0, 0.0
+            for (pw, _, pdata), rho in zip(pyr, modes):
+                rp = Runner(S, torch, pw.with_(density=rho if rho is not None else pw.density), *pdata,
+                            rho if rho is not None else pw.density)
+                dn_ms = float(np.median(rp.timed(rp.dense, 2)))
+                if rho is not None:
+                    ms = float(np.median(rp.timed(lambda: (rp.score(), rp.sparse()), 3)))
+                    fl = rp.flops()
+                else:
+                    ms, fl = dn_ms, rp.dense_flops()
+                total += ms
+                dense_total += dn_ms
+                scales.append({"lq": pw.lq, "lk": pw.lk, "density": rho, "mode": "dense" if rho is None else "sparse",
+                               "ms": ms, "dense_ms": dn_ms, "executed_tflop": fl / 1e12})
+                log(f"  Lq={pw.lq}: {'dense' if rho is None else f'rho={rho}'} {ms:.2f} ms (dense {dn_ms:.2f} ms)")
+                del rp
+            out[leg] = {"total_ms": total, "all_dense_ms": dense_total, "speedup_vs_all_dense": dense_total / total,
+                        "scales": scales}
 
     if not args.no_cpu_baseline:
-        log("cpu baseline (oracle on a bounded sample)")
-        num_h0 = counts[0, 0]
-        idx_h0 = r.idx[0, 0].cpu().numpy()
-        lists_h0 = [idx_h0[i, : num_h0[i]].tolist() for i in range(Lq // w.block)]
-        out["cpu_baseline"] = cpu_baseline(w, *data, r.keep, flops, lists_h0)
-        log(f"cpu baseline {out['cpu_baseline']['value']:.4f} TFLOP/s")
+        log("cpu baseline (the oracle on a bounded sample, extrapolated)")
+        import oracle as O
+
+        seg = w.segments()
+        keep_ref = O.keep_ranges_for_clip(2, seg["text"], seg["ref"])
+        out["cpu_baseline"] = cpu_baseline(w, *data, keep_ref, flops, r.idx.cpu().numpy(), counts)
+        log(f"cpu baseline {out['cpu_baseline']['value']:.4f} TFLOP/s ({out['cpu_baseline']['sample']})")
 
     print(json.dumps(out), flush=True)
     return 0

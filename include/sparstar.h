@@ -25,15 +25,18 @@
  *   - The caller owns every buffer.  The library allocates no device memory,
  *     copies nothing between host and device and never synchronises: each call
  *     validates its arguments on the host, enqueues its kernels on `stream`
- *     (a hipStream_t; NULL is the default stream) and returns.
+ *     (a hipStream_t passed as void*, so that this header needs no HIP
+ *     include; NULL is the default stream) and returns.
  *   - Return value: SPARSTAR_OK, or a negative code.  Argument errors are
  *     detected on the host before any HIP call (nothing is launched, outputs are
  *     untouched); a failed launch returns SPARSTAR_ERR_HIP.  Faults inside a
  *     kernel surface at the caller's next synchronisation, as for any HIP
  *     work.  sparstar_last_error() describes the last non-OK return on the
  *     calling thread.
- *   - The library holds no state besides that thread-local message; calls on
- *     different streams may run concurrently.
+ *   - The library holds no state besides that thread-local message and the
+ *     per-GPU scratch array of sparstar_score_blocks_static; calls on
+ *     different streams may run concurrently, except that calls of
+ *     sparstar_score_blocks_static on one GPU share that array.
  */
 #ifndef SPARSTAR_H
 #define SPARSTAR_H

@@ -804,12 +804,6 @@ static hipError_t launch_cfg(const AttnArgs& a, bool dense, hipStream_t stream) 
   return hipGetLastError();
 }
 
-size_t attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block) {
-  if (n_k < kSplits) return 0;  // fewer key blocks than ranges: single pass
-  const int64_t rows = bh * n_q * kSplits * block;
-  return attn_partial_o_bytes(rows, d) + size_t(rows) * 4 * sizeof(float);
-}
-
 hipError_t launch_attn(const AttnArgs& a, int d, int block, bool dense, hipStream_t stream) {
   if (d == 128 && block == 64) return launch_cfg<128, 64>(a, dense, stream);
   if (d == 128 && block == 128) return launch_cfg<128, 128>(a, dense, stream);

@@ -309,6 +309,12 @@ extern "C" int sparstar_score_blocks_fused(const void* q, const void* k, int B, 
                       kv_stride, nullptr, workspace, workspace_bytes, stream, true);
 }
 
+size_t sparstar::attn_workspace_bytes(int64_t bh, int64_t n_q, int64_t n_k, int d, int block) {
+  if (n_k < kSplits) return 0;  // fewer key blocks than ranges: single pass
+  const int64_t rows = bh * n_q * kSplits * block;
+  return attn_partial_o_bytes(rows, d) + size_t(rows) * 4 * sizeof(float);
+}
+
 extern "C" size_t sparstar_attn_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
   if (check_sizes(B, H, Lq, Lk, D, block_size) != SPARSTAR_OK) return 0;
   return sparstar::attn_workspace_bytes(int64_t(B) * H, ceil_div(Lq, block_size), ceil_div(Lk, block_size), D,

@@ -213,13 +213,35 @@ def _shm_worker(job):
             blk.close()
 
 
+def _may_spawn() -> bool:
+    """Whether worker processes may be started: not under a profiler (its
+    preloaded library would start GPU work in every child) and not after this
+    process has initialised the GPU through torch."""
+    import os
+    import sys
+
+    pre = os.environ.get("LD_PRELOAD", "")
+    if "rocprof" in pre or any(k.startswith(("ROCPROF", "ROCP_")) for k in os.environ):
+        return False
+    torch = sys.modules.get("torch")
+    if torch is not None:
+        try:
+            if torch.cuda.is_initialized():
+                return False
+        except Exception:  # pragma: no cover - a torch without cuda support
+            return False
+    return True
+
+
 def generate(w: Workload, heads: list[int] | None = None, workers: int | None = None):
     """Q [B, H', L_q, D], K and V [B, H', L_k, D] as bf16 bit patterns (uint16),
     for all heads or the listed ones (H' = len(heads)).
 
     Large workloads are generated by spawned worker processes (numpy's
-    generators hold the GIL) writing into shared memory; the result does not
-    depend on the number of workers."""
+    generators hold the GIL) writing into shared memory, unless a profiler is
+    attached or this process has already initialised the GPU: then everything
+    is generated in-process.  The result does not depend on the number of
+    workers."""
     import os
 
     hs = list(range(w.heads)) if heads is None else list(heads)
@@ -229,7 +251,7 @@ def generate(w: Workload, heads: list[int] | None = None, workers: int | None = 
     total = sum(int(np.prod(s)) for s in shapes) * 2
     if workers is None:
         workers = min(16, len(os.sched_getaffinity(0)), len(jobs))
-    if workers <= 1 or total < (256 << 20):
+    if workers <= 1 or total < (256 << 20) or not _may_spawn():
         out = [np.empty(s, dtype=np.uint16) for s in shapes]
         for b, hi, h in jobs:
             for dst, src in zip(out, generate_head(w, b, h)):
@@ -262,10 +284,3 @@ def head_densities(w: Workload, density: float | None = None) -> np.ndarray:
     r = np.random.default_rng([w.seed + 1000])
     lo, hi = (1.0 - w.density_spread) * rho, (1.0 + w.density_spread) * rho
     return np.clip(r.uniform(lo, hi, size=w.heads), 0.0, 1.0)
-
-
-def keep_ranges(w: Workload, clip: int = 2) -> list[tuple[int, int]]:
-    """The forced ranges of the workload: the text segment for a later clip, text
-    and reference for clip 1."""
-    seg = w.segments()
-    return [seg["text"]] if clip >= 2 else [seg["text"], seg["ref"]]

@@ -15,6 +15,19 @@ O_REL_FRO = 1e-2    # output: per-head relative Frobenius error
 LSE_ABS = 1e-3
 
 
+def keep_for(lib, w, clip: int = 2):
+    """Eq. 3's forced token ranges for the workload's text and reference
+    segments: (the library's, sparstar_clip_keep_ranges, for the GPU calls; the
+    oracle's, keep_ranges_for_clip, for the oracle calls).  They must agree."""
+    import oracle as O
+
+    seg = w.segments()
+    k_lib = lib.sparstar_clip_keep_ranges(clip, seg["text"], seg["ref"])
+    k_ref = O.keep_ranges_for_clip(clip, seg["text"], seg["ref"])
+    assert [tuple(r) for r in k_lib] == [tuple(r) for r in k_ref], (k_lib, k_ref)
+    return k_lib, k_ref
+
+
 def to_dev(bits: np.ndarray):
     """bf16 bit patterns (uint16) -> a contiguous bf16 tensor on the GPU."""
     import torch

@@ -12,8 +12,8 @@ import sys
 import numpy as np
 import pytest
 
-from synthetic import TINY, generate, keep_ranges
-from tests.helpers import to_dev
+from synthetic import TINY, generate
+from tests.helpers import keep_for, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -33,7 +33,7 @@ def test_graph_replay_matches_eager(gpu_lib, split, fused):
     _say(f"[graph] H={w.heads} D={w.head_dim} Lq={w.lq} Lk={w.lk} split={split} fused={fused}")
     qb, kb, vb = generate(w)
     q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
-    keep = keep_ranges(w)
+    keep, _ = keep_for(S, w)
     B, H, Lq, D = q.shape
     Lk = k.shape[2]
     n_q = -(-Lq // w.block)

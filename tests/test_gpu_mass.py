@@ -25,8 +25,8 @@ import numpy as np
 import pytest
 
 import oracle as O
-from synthetic import P720, TINY, bf16_to_f64, generate, keep_ranges
-from tests.helpers import LSE_ABS, lists_from_device, to_dev
+from synthetic import P720, TINY, bf16_to_f64, generate
+from tests.helpers import keep_for, LSE_ABS, lists_from_device, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -87,7 +87,7 @@ def test_retained_mass_end_to_end_tiny(gpu_lib):
     w = TINY
     _say(f"[mass] end to end {w.name}: selector, sparse and dense forward, mass")
     (qb, kb, vb), (q, k, v) = _tiny_inputs(w)
-    keep = keep_ranges(w)
+    keep, _ = keep_for(gpu_lib, w)
     num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
     _, lse_sel = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
     _, lse_all = gpu_lib.sparstar_dense_attn_fwd(q, k, v, w.block)
@@ -180,7 +180,7 @@ def test_mass_at_720p_sampled(gpu_lib):
     _say(f"[mass] {w.name}: generating heads {heads}")
     qb, kb, vb = generate(w, heads=heads, workers=1)
     q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
-    keep = keep_ranges(w)
+    keep, _ = keep_for(gpu_lib, w)
     _say(f"[mass] {w.name}: selector, sparse and dense forward")
     num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
     _, lse_sel = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)

@@ -16,8 +16,8 @@ import numpy as np
 import pytest
 
 import oracle as O
-from synthetic import TINY, Workload, bf16_to_f64, generate, keep_ranges
-from tests.helpers import (LSE_ABS, LSE_ABS_SHARP, O_MAX_ABS, O_MAX_ABS_SHARP, bf16_tensor_to_f64, check_gap_rule, check_output,
+from synthetic import TINY, Workload, bf16_to_f64, generate
+from tests.helpers import (keep_for, LSE_ABS, LSE_ABS_SHARP, O_MAX_ABS, O_MAX_ABS_SHARP, bf16_tensor_to_f64, check_gap_rule, check_output,
                            lists_from_device, lists_to_device, to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -96,7 +96,7 @@ def test_selector_matches_oracle(gpu_lib, name, w, clip):
     qb_, kb_, _ = generate(w)
     if name in _SPREAD:
         qb_, kb_ = _times_pow2(qb_, 3), _times_pow2(kb_, 3)
-    keep = keep_ranges(w, clip)
+    keep, keep_ref = keep_for(gpu_lib, w, clip)
     q_d, k_d = to_dev(qb_), to_dev(kb_)
     # pool, score and select kernels, with S written out and without
     num, idx, scores, qbar, kbar = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density)
@@ -116,7 +116,7 @@ def test_selector_matches_oracle(gpu_lib, name, w, clip):
     for h in range(w.heads):
         q = bf16_to_f64(qb_[0, h])
         k = bf16_to_f64(kb_[0, h])
-        ol, s_ref, kk, keep_set = O.select(q, k, w.block, w.density, keep)
+        ol, s_ref, kk, keep_set = O.select(q, k, w.block, w.density, keep_ref)
         sel = O.selectable_blocks(keep_set, w.lk, w.block)
         np.testing.assert_allclose(qbar[0, h], O.pool(q, w.block), rtol=0, atol=1e-5)
         np.testing.assert_allclose(kbar[0, h][sel], O.pool(k, w.block)[sel], rtol=0, atol=1e-5)
@@ -135,12 +135,12 @@ def test_selector_per_head_budgets_and_edge_budgets(gpu_lib):
     w = TINY.with_(name="budgets", heads=5, seed=21)
     _say("[selector] per-head budgets {0, 1e-6, 0.37, 1, 0.5}")
     qb_, kb_, _ = generate(w)
-    keep = keep_ranges(w)
+    keep, keep_ref = keep_for(gpu_lib, w)
     budgets = [0.0, 1e-6, 0.37, 1.0, 0.5]
     num, idx, _, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, budgets, with_scores=False)
     lists = lists_from_device(num, idx)
     for h, rho in enumerate(budgets):
-        ol, s_ref, kk, keep_set = O.select(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), w.block, rho, keep)
+        ol, s_ref, kk, keep_set = O.select(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), w.block, rho, keep_ref)
         sel = O.selectable_blocks(keep_set, w.lk, w.block)
         for i, row in enumerate(lists[0][h]):
             check_gap_rule(row, s_ref[i], keep_set, sel, kk)
@@ -174,16 +174,16 @@ def test_selector_256_heads_with_per_head_budgets(gpu_lib):
     _say("[selector] 256 heads, per-head budgets")
     qb_, kb_, _ = generate(w)
     n_k = -(-w.lk // w.block)
-    keep = keep_ranges(w)
+    keep, keep_ref = keep_for(gpu_lib, w)
     budgets = [(h % 9) / 8 for h in range(w.heads)]  # 0, 1/8, ..., 1 repeating
     num, idx, _, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, budgets, with_scores=False)
     num = num.cpu().numpy()
-    keep_set = O.keep_blocks(keep, w.lk, w.block)
+    keep_set = O.keep_blocks(keep_ref, w.lk, w.block)
     n_sel = n_k - len(keep_set)
     for h in range(w.heads):
         assert (num[0, h] == len(keep_set) + O.budget_k(budgets[h], n_sel)).all(), h
     for h in (0, 7, 8, 100, 255):
-        _, s_ref, kk, ks = O.select(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), w.block, budgets[h], keep)
+        _, s_ref, kk, ks = O.select(bf16_to_f64(qb_[0, h]), bf16_to_f64(kb_[0, h]), w.block, budgets[h], keep_ref)
         sel = O.selectable_blocks(ks, w.lk, w.block)
         rows = idx[0, h].cpu().numpy()
         for i in range(rows.shape[0]):
@@ -201,7 +201,7 @@ def test_batch_of_two_end_to_end(gpu_lib, split):
     _say(f"[batch] B={w.batch} H={w.heads} Lq={w.lq} Lk={w.lk} split={split}")
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
-    keep = keep_ranges(w)
+    keep, keep_ref = keep_for(gpu_lib, w)
     budgets = [0.2, 0.3, 0.45]
     n_q = -(-w.lq // w.block)
     num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, budgets, keep)
@@ -213,7 +213,7 @@ def test_batch_of_two_end_to_end(gpu_lib, split):
     for b in range(w.batch):
         for h in range(w.heads):
             qh, kh, vh = (bf16_to_f64(x[b, h]) for x in (qb_, kb_, vb_))
-            _, s_ref, kk, keep_set = O.select(qh, kh, w.block, budgets[h], keep)
+            _, s_ref, kk, keep_set = O.select(qh, kh, w.block, budgets[h], keep_ref)
             sel = O.selectable_blocks(keep_set, w.lk, w.block)
             for i in range(n_q):
                 check_gap_rule(lists[b][h][i], s_ref[i], keep_set, sel, kk)
@@ -245,11 +245,11 @@ def test_selector_ties_prefer_lower_index(gpu_lib):
     # blocks 0..3 and 12..15 become copies of block 11 (selectable in the Eq. 1 layout)
     for j in list(range(0, 4)) + list(range(12, 16)):
         kb_[0, 0, j * blk:(j + 1) * blk] = kb_[0, 0, 11 * blk:12 * blk]
-    keep = keep_ranges(w)
+    keep, keep_ref = keep_for(gpu_lib, w)
     num, idx, scores, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, 3 / 16)
     lists = lists_from_device(num, idx)[0][0]
     s = scores.cpu().numpy()[0, 0]
-    keep_set = O.keep_blocks(keep, w.lk, w.block)
+    keep_set = O.keep_blocks(keep_ref, w.lk, w.block)
     sel = O.selectable_blocks(keep_set, w.lk, w.block)
     for i, row in enumerate(lists):
         # the GPU's own fp32 scores decide; equal scores must resolve to lower indices
@@ -365,14 +365,14 @@ def test_end_to_end_tiny_against_oracle(gpu_lib):
     _say("[e2e] tiny")
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
-    keep = keep_ranges(w)
+    keep, keep_ref = keep_for(gpu_lib, w)
     num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
     o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
     torch.cuda.synchronize()
     lists = lists_from_device(num, idx)[0]
     for h in range(w.heads):
         qh, kh, vh = (bf16_to_f64(x[0, h]) for x in (qb_, kb_, vb_))
-        ol, s_ref, kk, keep_set = O.select(qh, kh, w.block, w.density, keep)
+        ol, s_ref, kk, keep_set = O.select(qh, kh, w.block, w.density, keep_ref)
         assert lists[h] == ol  # tiny: every boundary gap is large
         o_ref, l_ref = O.sparse_attention(qh, kh, vh, ol, w.block)
         check_output(bf16_tensor_to_f64(o)[0, h][None], o_ref[None], lse.cpu().numpy()[0, h][None].astype(np.float64),
@@ -483,7 +483,7 @@ def test_split_agrees_with_single_pass(gpu_lib):
     _say("[split vs one pass]")
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
-    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, 0.3, keep_ranges(w))
+    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, 0.3, keep_for(gpu_lib, w)[0])
     o1, l1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, split=True)
     o2, l2 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, split=False)
     torch.cuda.synchronize()
@@ -500,7 +500,7 @@ def test_deterministic(gpu_lib):
     _say("[determinism]")
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
-    keep = keep_ranges(w)
+    keep, keep_ref = keep_for(gpu_lib, w)
     r1 = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
     r2 = gpu_lib.sparstar_score_blocks(q, k, w.block, w.density, keep)
     o1 = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, *r1, w.block)
@@ -534,7 +534,7 @@ def test_empty_query_sequence_is_noop(gpu_lib):
     qb_, kb_, vb_ = generate(w)
     q = torch.empty((1, w.heads, 0, w.head_dim), dtype=torch.bfloat16, device="cuda")
     k, v = to_dev(kb_), to_dev(vb_)
-    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, 0.25, keep_ranges(w))
+    num, idx = gpu_lib.sparstar_score_blocks(q, k, w.block, 0.25, keep_for(gpu_lib, w)[0])
     o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block)
     torch.cuda.synchronize()
     assert o.numel() == 0 and num.numel() == 0
@@ -586,7 +586,7 @@ def test_selector_writes_only_its_list_entries(gpu_lib, fused):
     w = ATTN_CASES[1][1]
     _say(f"[guard] selector fused={fused}")
     qb_, kb_, _ = generate(w)
-    keep = keep_ranges(w)
+    keep, keep_ref = keep_for(gpu_lib, w)
     budgets = [0.1, 0.3, 0.6]
     n_q = -(-w.lq // w.block)
     stride = gpu_lib.sparstar_kv_stride(w.heads, w.lk, w.block, budgets, keep) + 5
@@ -598,7 +598,7 @@ def test_selector_writes_only_its_list_entries(gpu_lib, fused):
     assert _guards_intact(nbuf, nn) and _guards_intact(ibuf, ni), "a write outside the outputs"
     canary = np.frombuffer(bytes([_CANARY] * 4), dtype=np.int32)[0]
     n, ix = num.cpu().numpy(), idx.cpu().numpy()
-    keep_set = O.keep_blocks(keep, w.lk, w.block)
+    keep_set = O.keep_blocks(keep_ref, w.lk, w.block)
     n_sel = -(-w.lk // w.block) - len(keep_set)
     for h, rho in enumerate(budgets):
         c = len(keep_set) + O.budget_k(rho, n_sel)

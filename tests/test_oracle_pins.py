@@ -162,12 +162,13 @@ def test_topk_ties_prefer_lower_index():
 def test_select_tiny_planted_blocks_are_recovered():
     """On the tiny workload every query block's 3 planted key blocks must be
     among its 4 selected blocks (the planted offset dominates the score)."""
-    from synthetic import TINY, bf16_to_f64, generate_head, keep_ranges
+    from synthetic import TINY, bf16_to_f64, generate_head
     from synthetic.workloads import _band_blocks, _plant_candidates, _rng  # recipe replay
 
     w = TINY
     q, k, _ = generate_head(w, 0, 0)
-    lists, s, kk, keep = O.select(bf16_to_f64(q), bf16_to_f64(k), w.block, w.density, keep_ranges(w))
+    # the configuration's forced context: the text segment
+    lists, s, kk, keep = O.select(bf16_to_f64(q), bf16_to_f64(k), w.block, w.density, [w.segments()["text"]])
     assert keep == [8, 9] and kk == 4
     # replay the plant stream to recover the planted blocks
     rp = _rng(w, 0, 0, 3)
