@@ -75,15 +75,22 @@ def traffic_from_profile() -> dict | None:
 
 
 def _cpu_model() -> str:
-    """The host CPU's model name (from /proc/cpuinfo where there is one)."""
+    """The host CPU's model name with its family/model/stepping numbers (from
+    /proc/cpuinfo where there is one)."""
+    fields = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if ":" in line:
+                    k, v = (x.strip() for x in line.split(":", 1))
+                    fields.setdefault(k, v)
+                if not line.strip() and fields:
+                    break
     except OSError:
         pass
-    return platform.processor() or platform.machine()
+    name = fields.get("model name") or platform.processor() or platform.machine()
+    ids = [f"{k} {fields[k]}" for k in ("cpu family", "model", "stepping") if k in fields]
+    return f"{name} ({', '.join(ids)})" if ids else name
 
 
 CPU_SELECTOR_HEADS = (0, 12)   # heads whose whole selector the oracle runs
