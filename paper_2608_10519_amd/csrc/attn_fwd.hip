@@ -21,9 +21,11 @@
 //     the B-operand layout P^T needs -- so the softmax state is lane-local up to
 //     one cross-half (lane l <-> l+32) max per step (v_permlane32_swap);
 //   * online softmax in the log2 domain: the scale is folded into one FMA, the
-//     exponential is the bare v_exp_f32, and O is rescaled lazily, only when a
-//     query's running maximum grows by more than 2^8 (P then stays <= 256,
-//     harmless in fp32 and bf16), which skips nearly all rescales;
+//     exponential is the bare v_exp_f32, and the running maximum is not taken
+//     per tile: P is formed against the current one, and only when some lane's
+//     sum of a sub-tile's P exceeds 2^8 (so that some p might) is the tile's
+//     max taken, O and the sums rescaled by a power of two, and P formed
+//     again -- nearly never after the first tiles;
 //   * O^T += V^T P^T on the same MFMA (P rounded to bf16 once).  The V^T
 //     operand comes straight from the row-major V tile through the LDS
 //     transpose read ds_read_b64_tr_b16 (in each 16-lane group, source lane s
@@ -426,23 +428,9 @@ void attn_fwd_kernel(AttnArgs a) {
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[kt][e]);
     return mx;
   };
-  // lazy rescaling: O and l are only rescaled when a query's running maximum
-  // grows by more than 2^8
-  auto apply_max = [&](float mx) {
-    mx = half_swap_max(mx) * sl2;
-    if (__any(mx > m_run + 8.0f)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-      le_run *= alpha;
-#pragma unroll
-      for (int t = 0; t < C::DT; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc_o[t][e] *= alpha;
-      m_run = m_new;
-    }
-  };
-  auto needs_mask = [&](int blk) { return blk < 0 || (int64_t)blk * C::KB + C::KB > a.lk; };
+  // tiles [0, n_whole) lie wholly below Lk; -1 (as unsigned) and the rest need the mask
+  const uint32_t n_whole = (uint32_t)(a.lk / C::KB);
+  auto needs_mask = [&](int blk) { return (uint32_t)blk >= n_whole; };
 
   if (cnt > 0) {
     // ---- prologue.  The loads follow the order of the steady state (K(j+4)
@@ -462,7 +450,7 @@ void attn_fwd_kernel(AttnArgs a) {
     __syncthreads();
     scores(ks0, acc_s);
     if (needs_mask(b0)) mask_tile(acc_s, b0);
-    apply_max(tile_max(acc_s));
+    m_run = half_swap_max(tile_max(acc_s)) * sl2;  // O and the sums are still zero
     __syncthreads();  // K slot 0 is free
     dma(kbase, b3, ks0, kdma, 64u);
     wait_vmcnt<3 * C::DPW>();  // K(1)
@@ -473,11 +461,11 @@ void attn_fwd_kernel(AttnArgs a) {
     //   A: the scores of tile t+1 on the matrix cores while the exponentials of
     //      tile t run; then V(t) is waited for, a barrier releases K slot
     //      (t+1) % 3, and K(t+4) is loaded into it (it has 2.5 steps to land);
-    //   B: O += P V of tile t and the running max of tile t+1; then K(t+2) is
-    //      waited for, a barrier releases V slot t % 2, and V(t+2) is loaded
-    //      into it (1.5 steps to land).
-    // Each phase is branch-free, and sched_group_barrier interleaves its MFMAs
-    // with its VALU work so that the latter hides under the matrix cores.
+    //   B: O += P V of tile t; then K(t+2) is waited for, a barrier releases V
+    //      slot t % 2, and V(t+2) is loaded into it (1.5 steps to land).
+    // Apart from the rare exact path of phase A, the phases are branch-free,
+    // and sched_group_barrier interleaves their MFMAs with their VALU work so
+    // that the latter hides under the matrix cores.
     int t = 0;
     auto step = [&](auto tc) {
       constexpr int T = decltype(tc)::value;
@@ -485,13 +473,38 @@ void attn_fwd_kernel(AttnArgs a) {
       uint16_t* const kr = kslot(std::integral_constant<int, KS>{});
       uint16_t* const vr = vslot(std::integral_constant<int, VS>{});
 
-      // ---- phase A
+      // ---- phase A, per 32-key sub-tile kt: the K reads and score MFMAs of
+      // tile t+1 interleaved with the exponentials of sub-tile kt of tile t.
+      // The running max is only refreshed when a sub-tile could break the
+      // bound p <= 2^8: a lane's sum of the sub-tile's P stays <= 2^8 whenever
+      // every p does, so a larger (or non-finite) sum in any lane sends the
+      // wave to the exact path -- the sub-tile's max, a rescale of O and both
+      // sums to it, and the sub-tile's P again (then p <= 1 there).
       f32x16 acc_n[C::KT];
-      const float neg_m = m_run == -INFINITY ? 0.f : -m_run;
       uint32_t pk[C::KT][8];  // bf16 pairs of P^T, per 32-key sub-tile
       float pf[C::KT][16];    // the same p in fp32, summed for lse in phase B (one sub-tile per step)
 #pragma unroll
       for (int kt = 0; kt < C::KT; ++kt) {
+        // exp2 offset -m; +inf for a query that has seen no key yet, which makes
+        // the sum non-finite and takes the exact path
+        const float neg_m = m_run == -INFINITY ? INFINITY : -m_run;
+        float st = 0.f;  // row sum of the sub-tile's bf16 P (the lane's keys)
+        float se = 0.f;  // with two sub-tiles per step: row sum of its fp32 p
+        auto exps = [&](float off) {
+#pragma unroll
+          for (int e = 0; e < 16; e += 2) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e], sl2, off));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e + 1], sl2, off));
+            pk[kt][e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
+            st = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][e / 2]), ones, st, false);
+            if constexpr (C::KT == 1) {
+              pf[kt][e] = p0;
+              pf[kt][e + 1] = p1;
+            } else {
+              se += p0 + p1;
+            }
+          }
+        };
         uint4 kf[C::DS];
 #pragma unroll
         for (int s = 0; s < C::DS; ++s) kf[s] = lds_u4(kr, koff[s] + kt * 32 * C::RB);
@@ -501,29 +514,14 @@ void attn_fwd_kernel(AttnArgs a) {
         for (int s = 0; s < C::DS; ++s)
           acc_n[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[s]), qf[s],
                                                               acc_n[kt], 0, 0, 0);
-#pragma unroll
-        for (int e = 0; e < 16; e += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e], sl2, neg_m));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(acc_s[kt][e + 1], sl2, neg_m));
-          pk[kt][e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){p0, p1}, bf16x2));
-          if constexpr (C::KT == 1) {
-            pf[kt][e] = p0;
-            pf[kt][e + 1] = p1;
-          } else {
-            le_run += p0 + p1;
-          }
-        }
-      }
-      if constexpr (C::DS == 8) {
-        // per 32-key sub-tile: its K reads, then 8 x (score MFMA + the VALU of
-        // the exponentials); sub-tiles one after the other keeps one
-        // sub-tile's K operands live at a time.  With two sub-tiles per step
-        // (64-key tiles) the K reads go four at a time and the fp32 row sum is
-        // taken here: both keep the wave under 256 VGPRs without spills.
-        constexpr int RG = C::KT == 1 ? 8 : 4;  // K reads per group
-        constexpr int VA = C::KT == 1 ? 5 : 7;  // VALU per score MFMA
-#pragma unroll
-        for (int kt = 0; kt < C::KT; ++kt) {
+        exps(neg_m);
+        if constexpr (C::DS == 8) {
+          // the K reads in groups of RG, then 8 x (score MFMA + VA VALU of the
+          // exponentials and row sums); with two sub-tiles per step (64-key
+          // tiles) the K reads go four at a time and the fp32 row sum is
+          // taken here: both keep the wave under 256 VGPRs without spills
+          constexpr int RG = C::KT == 1 ? 8 : 4;  // K reads per group
+          constexpr int VA = C::KT == 1 ? 6 : 8;  // VALU per score MFMA
 #pragma unroll
           for (int g = 0; g < 8 / RG; ++g) {
             __builtin_amdgcn_sched_group_barrier(0x100, RG, 0);
@@ -534,8 +532,47 @@ void attn_fwd_kernel(AttnArgs a) {
             }
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
+        if (__builtin_amdgcn_ballot_w64(!(st <= 256.f))) {
+          float mx = -INFINITY;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc_s[kt][e]);
+          mx = half_swap_max(mx) * sl2;
+          if (mx > m_run) {
+            // the max moves up by a whole number of binades (to >= mx), so the
+            // rescale is exact, also on the bf16 P of the step's earlier
+            // sub-tiles, which are not yet in O but already in l and le.  A
+            // jump past 2^128 (or the first key) drops the old terms, which
+            // are then below 2^-120 of the new ones.
+            float alpha = 0.f;
+            const float dm = mx - m_run;
+            if (dm > 128.f) {
+              m_run = mx;
+            } else {
+              const float k = ceilf(dm);
+              alpha = __builtin_amdgcn_ldexpf(1.f, -(int)k);
+              m_run += k;
+            }
+            l_run *= alpha;
+            le_run *= alpha;
+#pragma unroll
+            for (int d = 0; d < C::DT; ++d)
+#pragma unroll
+              for (int e = 0; e < 16; ++e) acc_o[d][e] *= alpha;
+#pragma unroll
+            for (int j = 0; j < kt; ++j)
+#pragma unroll
+              for (int i = 0; i < 8; ++i)
+                pk[j][i] = pack2_bf16(__uint_as_float(pk[j][i] << 16) * alpha,
+                                      __uint_as_float(pk[j][i] & 0xffff0000u) * alpha);
+          }
+          st = 0.f;
+          se = 0.f;
+          exps(m_run == -INFINITY ? 0.f : -m_run);
+        }
+        l_run += st;
+        if constexpr (C::KT != 1) le_run += se;
       }
-      __builtin_amdgcn_sched_barrier(0);  // the phase ends here
       wait_vmcnt<2 * C::DPW>();  // V(t)
       __syncthreads();
       dma(kbase, b4, kr, kdma, 64u);
@@ -565,43 +602,32 @@ void attn_fwd_kernel(AttnArgs a) {
             acc_o[dt] =
                 __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, acc_o[dt], 0, 0, 0);
           }
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[kt][4 * half + i]), ones, l_run,
-                                                    false);
           if constexpr (C::KT == 1) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) le_run += pf[kt][8 * half + i];
           }
         }
-      float mx = tile_max(acc_n);
       if constexpr (C::DT == 4) {
         // the first two MFMAs' V reads, then (P V MFMA + the V reads of the
         // MFMA two ahead + VB VALU) for all but the last two MFMAs, then
-        // 2 x (MFMA + VB VALU); the VALU work is the row sums (with one sub-tile
-        // per step the fp32 one too, here where the VALU is idle rather than
-        // among the exponentials of phase A) and the max of the next tile
-        constexpr int VB = C::KT == 1 ? 4 : 2;
+        // 2 x (MFMA + VB VALU); with one sub-tile per step the VALU work is the
+        // fp32 row sum, here where the VALU is idle rather than among the
+        // exponentials of phase A
+        constexpr int VB = C::KT == 1 ? 2 : 0;
         __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
         for (int i = 0; i < 8 * C::KT - 2; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
+          if constexpr (VB > 0) __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
         }
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
+          if constexpr (VB > 0) __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
         }
       }
-      if (t + 1 < ntiles) {
-        if (needs_mask(b1)) {
-          mask_tile(acc_n, b1);
-          mx = tile_max(acc_n);
-        }
-        apply_max(mx);
-      }
+      if (t + 1 < ntiles && needs_mask(b1)) mask_tile(acc_n, b1);
       __builtin_amdgcn_sched_barrier(0);
       wait_vmcnt<3 * C::DPW>();  // K(t+2)
       __syncthreads();
@@ -632,9 +658,14 @@ void attn_fwd_kernel(AttnArgs a) {
     wait_vmcnt<0>();  // loads past the end of the list still write LDS
   }
 
-  // ---- write O and lse
+  // ---- write O and lse.  The lane's row index is derived again from the lane
+  // id (v_mbcnt) rather than kept live over the loop, where every VGPR counts.
   l_run = half_swap_sum(l_run);  // both lane halves now hold the query's row sums
   le_run = half_swap_sum(le_run);
+  const int lane_o = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const int l32o = lane_o % 32, hho = lane_o / 32;
+  const int64_t row_o = (int64_t)qb * BLK + qs * 32 + l32o;
+  const bool row_ok = row_o < a.lq;
   if constexpr (SPLIT) {
     // Partial result of this key range: the unnormalised P V, scaled by a
     // power of two 2^-ex per query row so that its largest magnitude lies in
@@ -650,30 +681,30 @@ void attn_fwd_kernel(AttnArgs a) {
     if (amax > 0.f && amax <= 3.402823466e38f) ex = __builtin_amdgcn_frexp_expf(amax);
     ex = ex < -126 ? -126 : ex;
     const float sc = __builtin_amdgcn_ldexpf(1.0f, -ex);
-    if (q_ok) {
-      const int64_t prow = (work * kSplits + split) * BLK + qs * 32 + l32;
+    if (row_ok) {
+      const int64_t prow = (work * kSplits + split) * BLK + qs * 32 + l32o;
       _Float16* po = reinterpret_cast<_Float16*>(a.part_o) + prow * D;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int d = 32 * t + 8 * g + 4 * hh;
+          const int d = 32 * t + 8 * g + 4 * hho;
           f16x4 w;
 #pragma unroll
           for (int e = 0; e < 4; ++e) w[e] = (_Float16)(acc_o[t][4 * g + e] * sc);
           *reinterpret_cast<f16x4*>(po + d) = w;
         }
-      if (hh == 0)
+      if (hho == 0)
         reinterpret_cast<float4*>(a.part_meta)[prow] = make_float4(m_run, l_run, le_run, (float)ex);
     }
-  } else if (q_ok) {
+  } else if (row_ok) {
     const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    uint16_t* op = a.o + (bh * a.lq + q_row) * D;
+    uint16_t* op = a.o + (bh * a.lq + row_o) * D;
 #pragma unroll
     for (int t = 0; t < C::DT; ++t)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int d = 32 * t + 8 * g + 4 * hh;
+        const int d = 32 * t + 8 * g + 4 * hho;
         float o[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = acc_o[t][4 * g + e] * inv;
@@ -682,8 +713,8 @@ void attn_fwd_kernel(AttnArgs a) {
         w.y = pack2_bf16(o[2], o[3]);
         *reinterpret_cast<uint2*>(op + d) = w;
       }
-    if (a.lse != nullptr && hh == 0)
-      a.lse[bh * a.lq + q_row] = le_run > 0.f ? (m_run + log2f(le_run)) * 0.69314718055994530942f : -INFINITY;
+    if (a.lse != nullptr && hho == 0)
+      a.lse[bh * a.lq + row_o] = le_run > 0.f ? (m_run + log2f(le_run)) * 0.69314718055994530942f : -INFINITY;
   }
 }
 

@@ -16,7 +16,7 @@ import numpy as np
 import pytest
 
 import oracle as O
-from synthetic import TINY, Workload, bf16_to_f64, generate
+from synthetic import TINY, Workload, bf16_bits, bf16_to_f64, generate
 from tests.helpers import (keep_for, LSE_ABS, LSE_ABS_SHARP, O_MAX_ABS, O_MAX_ABS_SHARP, bf16_tensor_to_f64, check_gap_rule, check_output,
                            lists_from_device, lists_to_device, to_dev)
 
@@ -267,7 +267,8 @@ def test_selector_ties_prefer_lower_index(gpu_lib):
         assert len(row) == len(keep_set) + 3
 
 
-def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_override=None, split=True):
+def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_override=None, split=True,
+               k_override=None):
     """Run the sparse forward with given lists on all heads; return GPU and oracle outputs."""
     import torch
 
@@ -276,6 +277,8 @@ def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_ove
         vb_ = v_override(vb_)
     if q_override is not None:
         qb_ = q_override(qb_)
+    if k_override is not None:
+        kb_ = k_override(kb_)
     n_q = -(-w.lq // w.block)
     _assert_splits(gpu_lib, w, split)
     num, idx = lists_to_device([lists_h], n_q)
@@ -556,6 +559,51 @@ def test_value_magnitudes_far_outside_fp16(gpu_lib, e, split):
     assert np.array_equal(og, og0 * 2.0 ** e), "O does not scale exactly with V"
     assert np.array_equal(lg, lg0), "lse depends on the scale of V"
     check_output(og * 2.0 ** -e, o_ref * 2.0 ** -e, lg, l_ref, what=f"V x 2^{e}")
+
+
+def _group_offsets(n_groups: int) -> np.ndarray:
+    """Logit offset (about one unit = one binade at D = 128) of each 32-key
+    group: in every run of four groups a rise of 20, a fall to +5, a fall to
+    -10, on a base that climbs 6 per run, and from group 50 on everything 150
+    higher (a jump past 2^128)."""
+    g = np.arange(n_groups)
+    c = 6.0 * (g // 4) + np.array([0.0, 20.0, 5.0, -10.0])[g % 4]
+    return c + np.where(g >= 50, 150.0, 0.0)
+
+
+@pytest.mark.parametrize("block", [64, 128])
+@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
+def test_running_max_jumps(gpu_lib, block, split):
+    """Logits that rise along every list by a few, by tens and, once, by 150
+    binades (Eq. 7's softmax over them).  The kernel forms P against its
+    running max and moves that max only when a 32-key sub-tile's P could pass
+    2^8: small rises stay on the fast path with p up to 2^8, larger ones take
+    the exact path (a power-of-two rescale of O and both row sums, and at
+    b = 128 of the bf16 P of the step's first sub-tile when its second one
+    rises), and the 150-binade jump drops the old terms.  O and lse must match
+    the oracle as on ordinary inputs."""
+    w = TINY.with_(name="jumps", head_dim=128, block=block, lq=300, l_ref=1700, l_text=200, heads=2, seed=23)
+    rng = np.random.default_rng(29 + block)
+
+    def q_over(qb):
+        q = 0.25 + 0.02 * rng.standard_normal(qb.shape).astype(np.float32)
+        return bf16_bits(q)
+
+    def k_over(kb):
+        n_groups = -(-w.lk // 32)
+        c = np.repeat(_group_offsets(n_groups), 32)[: w.lk].astype(np.float32)
+        k = rng.standard_normal(kb.shape).astype(np.float32) + 0.25 * c[None, None, :, None]
+        return bf16_bits(k)
+
+    lists_h = _random_lists(w, np.random.default_rng(31 + block))
+    lists_h[0][0] = list(range(-(-w.lk // w.block)))  # one query block sees every key block
+    _say(f"[jumps] b={block} split={split}")
+    og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, split=split, q_override=q_over, k_override=k_over)
+    assert np.isfinite(og).all() and np.isfinite(lg).all()
+    # the logits reach about 300 binades: lse is large, and its fp32 value is
+    # compared at the same absolute tolerance as everywhere else
+    assert l_ref.max() > 150.0
+    check_output(og, o_ref, lg, l_ref, what=f"jumps b={block}")
 
 
 _CANARY = 0x5A  # byte pattern of untouched guard memory
