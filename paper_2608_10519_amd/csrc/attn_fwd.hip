@@ -627,6 +627,9 @@ void attn_fwd_kernel(AttnArgs a) {
           if constexpr (VB > 0) __builtin_amdgcn_sched_group_barrier(0x002, VB, 0);
         }
       }
+      // keeps the fp32 row sum in this phase, among the P V MFMAs, rather than
+      // sunk into the next step ahead of its first score MFMA
+      if constexpr (C::KT == 1) asm volatile("" : "+v"(le_run));
       if (t + 1 < ntiles && needs_mask(b1)) mask_tile(acc_n, b1);
       __builtin_amdgcn_sched_barrier(0);
       wait_vmcnt<3 * C::DPW>();  // K(t+2)
