@@ -68,9 +68,11 @@ enum {
 
 /*
  * Bytes of device scratch sparstar_score_blocks needs for these sizes: the
- * pooled blocks qbar [B,H,n_q,D] and kbar [B,H,n_k,D] and the score matrix
- * S [B,H,n_q,n_k], all fp32, each region 256-byte aligned.  Returns 0 for
- * invalid sizes.
+ * pooled blocks qbar [B,H,n_q,D] and kbar [B,H,n_k,D] (4 bytes per element:
+ * each block is kept as a power-of-two scale times a pair of fp16 parts), the
+ * blocks' scales (int32, [B,H,n_q] and [B,H,n_k]) and the fp32 score matrix
+ * S [B,H,n_q,n_k], each region 256-byte aligned.  Returns 0 for invalid
+ * sizes.
  */
 size_t sparstar_score_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size);
 
@@ -131,8 +133,8 @@ int sparstar_score_blocks(const void* q, const void* k, int B, int H, int64_t Lq
  * qbar and kbar, and S when `scores` is NULL) lives in a device array of
  * SPARSTAR_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on
  * until the process ends.  With `scores` given, S goes there and only
- * qbar + kbar use the scratch (41.6 MB at 24 heads, 72,000 queries and
- * 144,512 keys in 64-token blocks); sizes that need more than the scratch
+ * qbar + kbar and their scales use the scratch (41.9 MB at 24 heads, 72,000
+ * queries and 144,512 keys in 64-token blocks); sizes that need more than the scratch
  * return SPARSTAR_ERR_WORKSPACE before any HIP call.
  *   - The call allocates nothing: no hipMalloc, hipFree or allocating library
  *     routine.  The first call on a device looks up the array's device address

@@ -182,8 +182,10 @@ extern "C" int sparstar_scale_densities(const int64_t* scale_lq, int n_scales, c
 
 extern "C" const char* sparstar_last_error(void) { return g_error.c_str(); }
 
+// Selector workspace: the pooled blocks split into fp16 hi and lo parts (4 D
+// bytes per block), their power-of-two scales, then S.
 struct WsLayout {
-  size_t q_bar, k_bar, s, total;
+  size_t q_bar, k_bar, q_exp, k_exp, s, total;
 };
 
 static WsLayout ws_layout(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
@@ -191,8 +193,10 @@ static WsLayout ws_layout(int B, int H, int64_t Lq, int64_t Lk, int D, int block
   const int64_t nq = ceil_div(Lq, block_size), nk = ceil_div(Lk, block_size);
   WsLayout w;
   w.q_bar = 0;
-  w.k_bar = align256(size_t(bh * nq * D) * sizeof(float));
-  w.s = w.k_bar + align256(size_t(bh * nk * D) * sizeof(float));
+  w.k_bar = align256(size_t(bh * nq * D) * 4);
+  w.q_exp = w.k_bar + align256(size_t(bh * nk * D) * 4);
+  w.k_exp = w.q_exp + align256(size_t(bh * nq) * sizeof(int32_t));
+  w.s = w.k_exp + align256(size_t(bh * nk) * sizeof(int32_t));
   w.total = w.s + align256(size_t(bh * nq * nk) * sizeof(float));
   return w;
 }
@@ -245,25 +249,28 @@ static int score_common(const void* q, const void* k, int B, int H, int64_t Lq, 
 
   const int bh = B * H;
   char* ws = static_cast<char*>(workspace);
-  float* q_bar = reinterpret_cast<float*>(ws + wl.q_bar);
-  float* k_bar = reinterpret_cast<float*>(ws + wl.k_bar);
+  uint16_t* q_bar = reinterpret_cast<uint16_t*>(ws + wl.q_bar);
+  uint16_t* k_bar = reinterpret_cast<uint16_t*>(ws + wl.k_bar);
+  int32_t* q_exp = reinterpret_cast<int32_t*>(ws + wl.q_exp);
+  int32_t* k_exp = reinterpret_cast<int32_t*>(ws + wl.k_exp);
   float* s = scores ? scores : reinterpret_cast<float*>(ws + wl.s);
   hipStream_t st = static_cast<hipStream_t>(stream);
 
-  PoolArgs pa{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), q_bar, k_bar, Lq, Lk, bh, int(nq),
-              int(nk), kb};
+  PoolArgs pa{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), q_bar, k_bar, q_exp, k_exp, Lq, Lk,
+              bh, int(nq), int(nk), kb};
   hipError_t e = launch_pool(pa, D, block_size, st);
   if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "pool launch: %s", hipGetErrorString(e));
   const float tau = float(1.0 / sqrt(double(D)));
   if (fused) {
     // scores and selection in one kernel, S kept in LDS
-    ScoreSelectArgs fa{q_bar, k_bar, kv_num_blocks, kv_indices, bh, int(nq), int(nk), H, kv_stride, D, tau, kb, hb};
+    ScoreSelectArgs fa{q_bar, k_bar, q_exp, k_exp, kv_num_blocks, kv_indices, bh, int(nq), int(nk), H, kv_stride, D,
+                       tau, kb, hb};
     e = launch_score_select(fa, st);
     if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "score/select launch: %s", hipGetErrorString(e));
     return ok();
   }
   if (n_sel > 0) {
-    ScoreArgs sa{q_bar, k_bar, s, bh, int(nq), int(nk), tau, kb};
+    ScoreArgs sa{q_bar, k_bar, q_exp, k_exp, s, bh, int(nq), int(nk), tau, kb};
     e = launch_score(sa, D, st);
     if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "score launch: %s", hipGetErrorString(e));
   }

@@ -22,20 +22,30 @@ struct HeadBudgets {
   int k[kMaxHeads];
 };
 
+// Pooled blocks are stored split for the fp16 matrix cores: row i of qbar (and
+// of kbar) is 2^e_i (hi_i + lo_i) with hi_i = fp16(2^-e_i qbar_i), lo_i =
+// fp16(2^-e_i qbar_i - hi_i) and e_i chosen so that the row's largest
+// magnitude scales into [2^13, 2^14): hi + lo carries 22 significant bits.
+// Layout per row: D fp16 hi values, then D fp16 lo values; e_i in its own
+// int32 array.
 struct PoolArgs {
   const uint16_t* q;  // [BH, Lq, D] bf16
   const uint16_t* k;  // [BH, Lk, D] bf16
-  float* q_bar;       // [BH, n_q, D]
-  float* k_bar;       // [BH, n_k, D]
+  uint16_t* q_bar;    // [BH, n_q, 2 D] fp16 (hi, lo)
+  uint16_t* k_bar;    // [BH, n_k, 2 D] fp16 (hi, lo)
+  int32_t* q_exp;     // [BH, n_q]
+  int32_t* k_exp;     // [BH, n_k]
   int64_t lq, lk;
   int bh, n_q, n_k;
   KeepBlocks keep;    // key blocks that are never pooled or scored
 };
 
 struct ScoreArgs {
-  const float* q_bar;  // [BH, n_q, D]
-  const float* k_bar;  // [BH, n_k, D]
-  float* s;            // [BH, n_q, n_k]
+  const uint16_t* q_bar;  // [BH, n_q, 2 D] fp16 (hi, lo)
+  const uint16_t* k_bar;  // [BH, n_k, 2 D] fp16 (hi, lo)
+  const int32_t* q_exp;   // [BH, n_q]
+  const int32_t* k_exp;   // [BH, n_k]
+  float* s;               // [BH, n_q, n_k]
   int bh, n_q, n_k;
   float tau;           // D^-1/2
   KeepBlocks keep;
@@ -58,8 +68,10 @@ constexpr int kFusedRows = 16;
 constexpr int kFusedMaxBlocks = 2304;
 
 struct ScoreSelectArgs {
-  const float* q_bar;      // [BH, n_q, D]
-  const float* k_bar;      // [BH, n_k, D]
+  const uint16_t* q_bar;   // [BH, n_q, 2 D] fp16 (hi, lo)
+  const uint16_t* k_bar;   // [BH, n_k, 2 D] fp16 (hi, lo)
+  const int32_t* q_exp;    // [BH, n_q]
+  const int32_t* k_exp;    // [BH, n_k]
   int32_t* kv_num_blocks;  // [BH, n_q]
   int32_t* kv_indices;     // [BH, n_q, stride]
   int bh, n_q, n_k, heads, stride, d;

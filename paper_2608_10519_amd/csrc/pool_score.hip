@@ -3,10 +3,14 @@
 // pool:  qbar_i = b^-1 sum_r q~_{i,r}, kbar_j likewise; the final partial block
 //        is zero-padded and still divided by the nominal b.  One work-group per
 //        block streams its b x D bf16 tile once with 16-byte loads (HBM-bound;
-//        algorithmic bytes = 2*D per token read + 4*D per block written).
-// score: S_ij = tau * qbar_i . kbar_j in fp32 (MFMA) for selectable j; forced key
-//        blocks are neither pooled nor scored (Section 5.2), their S columns are
-//        left untouched.
+//        algorithmic bytes = 2*D per token read + 4*D + 4 per block written).
+//        The mean is written split for the fp16 matrix cores (launch.h):
+//        2^e (hi + lo) with e the row's power-of-two scale.
+// score: S_ij = tau * qbar_i . kbar_j for selectable j, on fp16 MFMA with
+//        fp32 accumulation as hi.hi + hi.lo + lo.hi: the dropped lo.lo term
+//        and the split leave a relative error near 2^-21 of sum |q k|, the
+//        level of an fp32 dot product; forced key blocks are neither pooled
+//        nor scored (Section 5.2), their S columns are left untouched.
 #include "device_common.h"
 
 namespace sparstar {
@@ -22,6 +26,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   constexpr int RG = 256 / CH;
   constexpr int RPT = BLK / RG;
   __shared__ float red[RG][D + 1];
+  __shared__ float wmax[4];
 
   const int64_t wg = blockIdx.x;
   const int64_t nqb = (int64_t)a.bh * a.n_q;
@@ -63,36 +68,57 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) red[g][c * 8 + e] = acc[e];
   __syncthreads();
+  float x = 0.f;  // element t of the block mean
   if (t < D) {
     float s = 0.f;
 #pragma unroll
     for (int r = 0; r < RG; ++r) s += red[r][t];
-    float* dst = (is_q ? a.q_bar : a.k_bar) + (bh * nb + blk) * D;
-    dst[t] = s * (1.0f / BLK);
+    x = s * (1.0f / BLK);
   }
+  // the row's largest magnitude (a wave maximum, then over the four waves)
+  // fixes its scale 2^e: |x| 2^-e < 2^14, inside fp16's range
+  float m = fabsf(x);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+  if (t % 64 == 0) wmax[t / 64] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+  const int ex = (m > 0.f && m <= 3.402823466e38f) ? __builtin_amdgcn_frexp_expf(m) - 14 : 0;
+  const int64_t row = bh * nb + blk;
+  if (t < D) {
+    const float xs = __builtin_amdgcn_ldexpf(x, -ex);
+    const _Float16 hi = (_Float16)xs;
+    const _Float16 lo = (_Float16)(xs - (float)hi);  // the difference is exact in fp32
+    uint16_t* dst = (is_q ? a.q_bar : a.k_bar) + row * (2 * D);
+    dst[t] = __builtin_bit_cast(uint16_t, hi);
+    dst[D + t] = __builtin_bit_cast(uint16_t, lo);
+  }
+  if (t == 0) (is_q ? a.q_exp : a.k_exp)[row] = ex;
 }
 
 // ---------------------------------------------------------------------------
 // score: one work-group per (bh, 64 query blocks, 64 key blocks) tile of S,
-// four waves, each a 32 x 32 sub-tile on v_mfma_f32_32x32x2_f32 (fp32
-// products, fp32 accumulation).  D is streamed through LDS in chunks of SKC
-// columns (coalesced 16-byte loads), which keeps a work-group at 18 KB of LDS
-// so that many share a CU; rows are padded by 4 floats, which makes the
-// per-lane row reads below free of bank conflicts.
+// four waves, each a 32 x 32 sub-tile on v_mfma_f32_32x32x16_f16.  D is
+// streamed through LDS in chunks of SKC columns (16-byte loads of the hi and
+// lo parts), each LDS row holding the chunk's hi then lo values of one pooled
+// row, padded to 144 bytes: 16 consecutive rows read at one 16-byte offset
+// then fall on 16 disjoint groups of four banks.  The next chunk's loads are
+// in flight while the current chunk is multiplied.
 //
 // MFMA operands (lane l, h = l / 32): A[m][k] = qbar[m = l % 32][d],
-// B[k][n] = kbar[n = l % 32][d] with k = h; within a chunk MFMA s reads
-// d = (SKC/2) h + s, so each lane walks its own half-row with 16-byte reads.
-// C[m][n] sits at accumulator a with n = l % 32, m = 8 (a / 4) + 4 h + (a % 4).
+// B[k][n] = kbar[n = l % 32][d], k = 8 h + i over the lane's 8 fp16 values at
+// d = 16 s + 8 h + i of k-step s.  C[m][n] sits at accumulator a with
+// n = l % 32, m = 8 (a / 4) + 4 h + (a % 4).
 // ---------------------------------------------------------------------------
 constexpr int ST = 64;   // tile edge (query blocks and key blocks)
 constexpr int SKC = 32;  // D chunk
 
 template <int D>
 __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
-  constexpr int RS = SKC + 4;  // padded LDS row (floats)
-  __shared__ __attribute__((aligned(16))) float qs[ST * RS];
-  __shared__ __attribute__((aligned(16))) float ks[ST * RS];
+  constexpr int RB = 144;  // padded LDS row (bytes): SKC hi + SKC lo fp16
+  __shared__ __attribute__((aligned(16))) unsigned char qs[ST * RB];
+  __shared__ __attribute__((aligned(16))) unsigned char ks[ST * RB];
+  __shared__ int qe[ST], ke[ST];
   const int tiles_i = (a.n_q + ST - 1) / ST;
   const int tiles_j = (a.n_k + ST - 1) / ST;
   int64_t wg = blockIdx.x;
@@ -102,27 +128,23 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   const int64_t bh = wg / tiles_i;
   const int i0 = ti * ST, j0 = tj * ST;
 
-  const float* qb = a.q_bar + bh * (int64_t)a.n_q * D;
-  const float* kb = a.k_bar + bh * (int64_t)a.n_k * D;
   const int t = threadIdx.x;
   const int wave = t / 64, lane = t % 64, l32 = lane % 32, h = lane / 32;
   const int wq = wave / 2, wk = wave % 2;  // the wave's 32 x 32 sub-tile
-  // loader: 64 rows x SKC floats = 512 float4 per tile; thread t loads rows lr and lr + 32.
-  // Rows past the end re-read a valid row and are zeroed when staged; the
-  // next chunk's loads are in flight while the current chunk is multiplied.
-  const int lr = t / 8, lc = (t % 8) * 4;
-  const bool q0_ok = i0 + lr < a.n_q, q1_ok = i0 + lr + 32 < a.n_q;
-  const bool k0_ok = j0 + lr < a.n_k, k1_ok = j0 + lr + 32 < a.n_k;
-  const float* const qr0 = qb + (int64_t)(q0_ok ? i0 + lr : 0) * D + lc;
-  const float* const qr1 = qb + (int64_t)(q1_ok ? i0 + lr + 32 : 0) * D + lc;
-  const float* const kr0 = kb + (int64_t)(k0_ok ? j0 + lr : 0) * D + lc;
-  const float* const kr1 = kb + (int64_t)(k1_ok ? j0 + lr + 32 : 0) * D + lc;
-  float4 q0 = *reinterpret_cast<const float4*>(qr0), q1 = *reinterpret_cast<const float4*>(qr1);
-  float4 k0 = *reinterpret_cast<const float4*>(kr0), k1 = *reinterpret_cast<const float4*>(kr1);
-  // element-wise (a select of whole float4 values goes through scratch memory)
-  auto keep_if = [](bool ok, float4 v) {
-    return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
+  // loader: thread t stages row lr, 16-byte piece lc of the chunk's hi and lo
+  // parts.  Rows past the end re-read a valid row and are zeroed when staged.
+  const int lr = t / 4, lc = t % 4;
+  const bool q_ok = i0 + lr < a.n_q, k_ok = j0 + lr < a.n_k;
+  const uint16_t* const qrow = a.q_bar + (bh * a.n_q + (q_ok ? i0 + lr : 0)) * (2 * D) + 8 * lc;
+  const uint16_t* const krow = a.k_bar + (bh * a.n_k + (k_ok ? j0 + lr : 0)) * (2 * D) + 8 * lc;
+  auto ld = [](const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); };
+  // element-wise (a select of whole uint4 values goes through scratch memory)
+  auto keep_if = [](bool ok, uint4 v) {
+    return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
   };
+  uint4 qh = ld(qrow), ql = ld(qrow + D), kh = ld(krow), kl = ld(krow + D);
+  if (t < ST) qe[t] = i0 + t < a.n_q ? a.q_exp[bh * a.n_q + i0 + t] : 0;
+  else if (t < 2 * ST) ke[t - ST] = j0 + t - ST < a.n_k ? a.k_exp[bh * a.n_k + j0 + t - ST] : 0;
 
   f32x16 acc;
 #pragma unroll
@@ -130,37 +152,40 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
 #pragma unroll
   for (int d0 = 0; d0 < D; d0 += SKC) {
     if (d0 > 0) __syncthreads();  // the previous chunk's reads are done
-    *reinterpret_cast<float4*>(qs + lr * RS + lc) = keep_if(q0_ok, q0);
-    *reinterpret_cast<float4*>(qs + (lr + 32) * RS + lc) = keep_if(q1_ok, q1);
-    *reinterpret_cast<float4*>(ks + lr * RS + lc) = keep_if(k0_ok, k0);
-    *reinterpret_cast<float4*>(ks + (lr + 32) * RS + lc) = keep_if(k1_ok, k1);
+    *reinterpret_cast<uint4*>(qs + lr * RB + 16 * lc) = keep_if(q_ok, qh);
+    *reinterpret_cast<uint4*>(qs + lr * RB + 64 + 16 * lc) = keep_if(q_ok, ql);
+    *reinterpret_cast<uint4*>(ks + lr * RB + 16 * lc) = keep_if(k_ok, kh);
+    *reinterpret_cast<uint4*>(ks + lr * RB + 64 + 16 * lc) = keep_if(k_ok, kl);
     __syncthreads();
     if (d0 + SKC < D) {
-      q0 = *reinterpret_cast<const float4*>(qr0 + d0 + SKC);
-      q1 = *reinterpret_cast<const float4*>(qr1 + d0 + SKC);
-      k0 = *reinterpret_cast<const float4*>(kr0 + d0 + SKC);
-      k1 = *reinterpret_cast<const float4*>(kr1 + d0 + SKC);
+      qh = ld(qrow + d0 + SKC);
+      ql = ld(qrow + D + d0 + SKC);
+      kh = ld(krow + d0 + SKC);
+      kl = ld(krow + D + d0 + SKC);
     }
-    const float* qa = qs + (wq * 32 + l32) * RS + (SKC / 2) * h;
-    const float* kc = ks + (wk * 32 + l32) * RS + (SKC / 2) * h;
+    const unsigned char* qa = qs + (wq * 32 + l32) * RB + 16 * h;
+    const unsigned char* kc = ks + (wk * 32 + l32) * RB + 16 * h;
 #pragma unroll
-    for (int i = 0; i < SKC / 8; ++i) {
-      const float4 x = *reinterpret_cast<const float4*>(qa + 4 * i);
-      const float4 y = *reinterpret_cast<const float4*>(kc + 4 * i);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.x, y.x, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.y, y.y, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.z, y.z, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.w, y.w, acc, 0, 0, 0);
+    for (int s = 0; s < SKC / 16; ++s) {
+      const f16x8 ah = *reinterpret_cast<const f16x8*>(qa + 32 * s);
+      const f16x8 al = *reinterpret_cast<const f16x8*>(qa + 64 + 32 * s);
+      const f16x8 bh_ = *reinterpret_cast<const f16x8*>(kc + 32 * s);
+      const f16x8 bl = *reinterpret_cast<const f16x8*>(kc + 64 + 32 * s);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, bh_, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, bl, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(al, bh_, acc, 0, 0, 0);
     }
   }
 
   const int j = j0 + wk * 32 + l32;
   if (j >= a.n_k || keep_block(a.keep, j)) return;  // no barrier below
+  const int ej = ke[wk * 32 + l32];
   float* scol = a.s + bh * (int64_t)a.n_q * a.n_k + j;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
-    const int i = i0 + wq * 32 + 8 * (e / 4) + 4 * h + (e % 4);
-    if (i < a.n_q) scol[(int64_t)i * a.n_k] = a.tau * acc[e];
+    const int r = wq * 32 + 8 * (e / 4) + 4 * h + (e % 4);
+    const int i = i0 + r;
+    if (i < a.n_q) scol[(int64_t)i * a.n_k] = a.tau * __builtin_amdgcn_ldexpf(acc[e], qe[r] + ej);
   }
 }
 

@@ -206,17 +206,15 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_reg_kernel(SelectArgs a
 // kFusedRows query blocks of one head goes into LDS as order keys, and each
 // wave then selects one row from there (Eq. 6), so S never leaves the CU.
 //
-// Scores on v_mfma_f32_16x16x4_f32 (fp32 products, fp32 accumulation): per
-// 16-key tile, A = kbar (16 keys x 4 d), B = qbar^T (4 d x 16 query blocks),
-// C = S^T (16 keys x 16 query blocks).  Lane l (g = l / 16) supplies
-// A[l % 16][g] and B[g][l % 16], and receives C[4 g + r][l % 16], r = 0..3:
-// four consecutive keys of one row, stored as one 16-byte LDS write.  The d
-// index is permuted consistently between A and B: MFMA s = 4 c + e reads
-// d = 16 c + 4 g + e, so that lane l loads its kbar (and qbar) row as float4 at
-// d = 16 c + 4 g and the four lanes of a row read 64 contiguous bytes per load.
-// The 16-key tiles go round-robin over the waves.  Work-groups are numbered
-// so that each XCD runs consecutive groups of query blocks (one head's kbar
-// at a time in its L2).
+// Scores on v_mfma_f32_16x16x32_f16 over the split pooled rows (hi.hi + hi.lo
+// + lo.hi, fp32 accumulation, as the separate score kernel): per 16-key tile,
+// A = kbar (16 keys x 32 d), B = qbar^T (32 d x 16 query blocks), C = S^T
+// (16 keys x 16 query blocks).  Lane l (g = l / 16) supplies the 8 fp16 values
+// d = 32 s + 8 g + i of key (A) or query block (B) l % 16, and receives
+// C[4 g + r][l % 16], r = 0..3: four consecutive keys of one row, stored as one
+// 16-byte LDS write.  The 16-key tiles go round-robin over the waves.
+// Work-groups are numbered so that each XCD runs consecutive groups of query
+// blocks (one head's kbar at a time in its L2).
 // ---------------------------------------------------------------------------
 template <int D, int C>
 __global__ __launch_bounds__(64 * kFusedRows) void score_select_kernel(ScoreSelectArgs a) {
@@ -228,57 +226,69 @@ __global__ __launch_bounds__(64 * kFusedRows) void score_select_kernel(ScoreSele
   const int i0 = (int)(wl % groups) * kFusedRows;
   const int row_len = (a.n_k + 15) / 16 * 16;  // whole 16-key tiles
 
-  constexpr int DC = D / 16;  // float4 loads per lane and row (d = 16 c + 4 g)
+  constexpr int KS = D / 32;  // k-steps
   const int n16 = lane % 16, g = lane / 16;
-  // B operand: qbar of query block i0 + n16, zeros past n_q
+  // B operand: qbar of query block i0 + n16 (hi and lo), zeros past n_q
   const int qi = i0 + n16;
-  const float* qrow = a.q_bar + (bh * a.n_q + (qi < a.n_q ? qi : 0)) * D;
-  float4 qf[DC];
+  const bool q_ok = qi < a.n_q;
+  const uint16_t* qrow = a.q_bar + (bh * a.n_q + (q_ok ? qi : 0)) * (2 * D);
+  // element-wise (a select of whole uint4 values goes through scratch memory)
+  auto keep_if = [](bool ok, uint4 v) {
+    return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+  };
+  uint4 qh[KS], ql[KS];
 #pragma unroll
-  for (int c = 0; c < DC; ++c)
-    qf[c] = qi < a.n_q ? *reinterpret_cast<const float4*>(qrow + 16 * c + 4 * g) : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s = 0; s < KS; ++s) {
+    const uint4 vh = *reinterpret_cast<const uint4*>(qrow + 32 * s + 8 * g);
+    const uint4 vl = *reinterpret_cast<const uint4*>(qrow + D + 32 * s + 8 * g);
+    qh[s] = keep_if(q_ok, vh);
+    ql[s] = keep_if(q_ok, vl);
+  }
+  const int eq = q_ok ? a.q_exp[bh * a.n_q + qi] : 0;
 
-  const float* kb = a.k_bar + bh * (int64_t)a.n_k * D;
+  const uint16_t* kb = a.k_bar + bh * (int64_t)a.n_k * (2 * D);
+  const int32_t* kexp = a.k_exp + bh * (int64_t)a.n_k;
   const int tiles = row_len / 16;
   // kbar rows of tile kt (zeros past n_k); the next tile's loads are issued
   // before the current tile's MFMAs
-  auto load_k = [&](int kt, float4 (&kf)[DC]) {
+  auto load_k = [&](int kt, uint4 (&kh)[KS], uint4 (&kl)[KS]) {
     const int kj = kt * 16 + n16;
     const bool ok = kt < tiles && kj < a.n_k;
-    const float* krow = kb + (int64_t)(ok ? kj : 0) * D;
+    const uint16_t* krow = kb + (int64_t)(ok ? kj : 0) * (2 * D);
 #pragma unroll
-    for (int c = 0; c < DC; ++c) {
-      const float4 v = *reinterpret_cast<const float4*>(krow + 16 * c + 4 * g);
-      kf[c] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < KS; ++s) {
+      const uint4 vh = *reinterpret_cast<const uint4*>(krow + 32 * s + 8 * g);
+      const uint4 vl = *reinterpret_cast<const uint4*>(krow + D + 32 * s + 8 * g);
+      kh[s] = keep_if(ok, vh);
+      kl[s] = keep_if(ok, vl);
     }
   };
-  float4 kn[DC];
-  load_k(wave, kn);
+  uint4 nh[KS], nl[KS];
+  load_k(wave, nh, nl);
   for (int kt = wave; kt < tiles; kt += kFusedRows) {
-    float4 kf[DC];
+    uint4 kh[KS], kl[KS];
 #pragma unroll
-    for (int c = 0; c < DC; ++c) kf[c] = kn[c];
-    load_k(kt + kFusedRows, kn);
-    // two independent accumulation chains (even and odd c), added at the end
-    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < DC; c += 2) {
-      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c].x, qf[c].x, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c + 1].x, qf[c + 1].x, acc1, 0, 0, 0);
-      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c].y, qf[c].y, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c + 1].y, qf[c + 1].y, acc1, 0, 0, 0);
-      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c].z, qf[c].z, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c + 1].z, qf[c + 1].z, acc1, 0, 0, 0);
-      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c].w, qf[c].w, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[c + 1].w, qf[c + 1].w, acc1, 0, 0, 0);
+    for (int s = 0; s < KS; ++s) {
+      kh[s] = nh[s];
+      kl[s] = nl[s];
     }
-    const f32x4 acc = acc0 + acc1;
+    load_k(kt + kFusedRows, nh, nl);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const f16x8 ah = __builtin_bit_cast(f16x8, kh[s]), al = __builtin_bit_cast(f16x8, kl[s]);
+      const f16x8 bh_ = __builtin_bit_cast(f16x8, qh[s]), bl = __builtin_bit_cast(f16x8, ql[s]);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh_, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh_, acc, 0, 0, 0);
+    }
     // keys 16 kt + 4 g + r of row n16; forced blocks and blocks past n_k get key 0
     uint32_t k4[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int j = 16 * kt + 4 * g + r;
-      k4[r] = (j < a.n_k && !keep_block(a.keep, j)) ? order_key(a.tau * acc[r]) : 0u;
+      const bool live = j < a.n_k && !keep_block(a.keep, j);
+      k4[r] = live ? order_key(a.tau * __builtin_amdgcn_ldexpf(acc[r], eq + kexp[live ? j : 0])) : 0u;
     }
     *reinterpret_cast<uint4*>(fused_keys + (size_t)n16 * row_len + 16 * kt + 4 * g) =
         make_uint4(k4[0], k4[1], k4[2], k4[3]);

@@ -38,9 +38,11 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_workspace_bytes(lib):
-    # 720p: qbar 24*1125*128*4, kbar 24*2258*128*4, S 24*1125*2258*4 (256-aligned regions)
+    # 720p: qbar 24*1125*128*4, kbar 24*2258*128*4, their scales 24*1125*4 and
+    # 24*2258*4, S 24*1125*2258*4 (256-aligned regions)
     al = lambda x: (x + 255) // 256 * 256
-    want = al(24 * 1125 * 128 * 4) + al(24 * 2258 * 128 * 4) + al(24 * 1125 * 2258 * 4)
+    want = (al(24 * 1125 * 128 * 4) + al(24 * 2258 * 128 * 4) + al(24 * 1125 * 4) + al(24 * 2258 * 4)
+            + al(24 * 1125 * 2258 * 4))
     assert S.sparstar_score_workspace_bytes(1, 24, 72_000, 144_512, 128, 64) == want
     assert S.sparstar_score_workspace_bytes(1, 24, 72_000, 144_512, 96, 64) == 0
     assert S.sparstar_score_workspace_bytes(0, 24, 72_000, 144_512, 128, 64) == 0

@@ -29,13 +29,22 @@ def _say(msg):
 
 
 def _ws_views(ws, B, H, n_q, n_k, D):
-    """Split the selector workspace into (q_bar, k_bar) views (layout in sparstar.h)."""
-    import torch
+    """The pooled blocks in the selector workspace (layout in sparstar.h): each
+    block is 2^e (hi + lo) with hi and lo fp16 and e an int32 scale.  Returns
+    them decoded as float64 arrays, q_bar [B,H,n_q,D] and k_bar [B,H,n_k,D]."""
+    al = lambda x: (x + 255) // 256 * 256
+    rq, rk = B * H * n_q, B * H * n_k
+    off_k = al(rq * D * 4)
+    off_qe = off_k + al(rk * D * 4)
+    off_ke = off_qe + al(rq * 4)
+    raw = ws.cpu().numpy()
 
-    f = ws.view(torch.float32)
-    qn = B * H * n_q * D
-    off_k = ((qn * 4 + 255) // 256 * 256) // 4
-    return f[:qn].view(B, H, n_q, D), f[off_k: off_k + B * H * n_k * D].view(B, H, n_k, D)
+    def decode(off, rows, off_e, n):
+        hl = raw[off: off + rows * D * 4].view(np.float16).reshape(rows, 2, D).astype(np.float64)
+        e = raw[off_e: off_e + rows * 4].view(np.int32).astype(np.float64)
+        return ((hl[:, 0] + hl[:, 1]) * np.exp2(e)[:, None]).reshape(B, H, n, D)
+
+    return decode(0, rq, off_qe, n_q), decode(off_k, rk, off_ke, n_k)
 
 
 def _times_pow2(bits: np.ndarray, e: int) -> np.ndarray:
@@ -45,7 +54,7 @@ def _times_pow2(bits: np.ndarray, e: int) -> np.ndarray:
     return bf16_bits((bf16_to_f64(bits) * 2.0 ** e).astype(np.float32))
 
 
-def _run_selector(lib, w: Workload, q, k, keep, budget, with_scores=True, fused=False):
+def _run_selector(lib, w: Workload, q, k, keep, budget, with_scores=True, fused=False, pooled=False):
     import torch
 
     B, H, Lq, D = q.shape
@@ -56,7 +65,7 @@ def _run_selector(lib, w: Workload, q, k, keep, budget, with_scores=True, fused=
     scores = torch.full((B, H, n_q, n_k), float("nan"), device="cuda") if with_scores else None
     num, idx = lib.sparstar_score_blocks(q, k, w.block, budget, keep, scores=scores, workspace=ws, fused=fused)
     torch.cuda.synchronize()
-    qb, kb = _ws_views(ws, B, H, n_q, n_k, D)
+    qb, kb = _ws_views(ws, B, H, n_q, n_k, D) if pooled else (None, None)
     return num, idx, scores, qb, kb
 
 
@@ -99,7 +108,7 @@ def test_selector_matches_oracle(gpu_lib, name, w, clip):
     keep, keep_ref = keep_for(gpu_lib, w, clip)
     q_d, k_d = to_dev(qb_), to_dev(kb_)
     # pool, score and select kernels, with S written out and without
-    num, idx, scores, qbar, kbar = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density)
+    num, idx, scores, qbar, kbar = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density, pooled=True)
     lists = lists_from_device(num, idx)
     num_n, idx_n, _, _, _ = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density, with_scores=False)
     assert lists_from_device(num_n, idx_n) == lists
@@ -110,7 +119,6 @@ def test_selector_matches_oracle(gpu_lib, name, w, clip):
         num_f, idx_f, _, _, _ = _run_selector(gpu_lib, w, q_d, k_d, keep, w.density, with_scores=False, fused=True)
         lists_f = lists_from_device(num_f, idx_f)
     s_gpu = scores.cpu().numpy()
-    qbar, kbar = qbar.cpu().numpy(), kbar.cpu().numpy()
     stats = {"exact": 0, "tolerant": 0}
     stats_f = {"exact": 0, "tolerant": 0}
     for h in range(w.heads):
