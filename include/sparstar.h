@@ -71,8 +71,8 @@ enum {
  * pooled blocks qbar [B,H,n_q,D] and kbar [B,H,n_k,D] (4 bytes per element:
  * each block is kept as a power-of-two scale times a pair of fp16 parts), the
  * blocks' scales (int32, [B,H,n_q] and [B,H,n_k]) and the fp32 score matrix
- * S [B,H,n_q,n_k], each region 256-byte aligned.  Returns 0 for invalid
- * sizes.
+ * S [B,H,n_q,n_k] with its rows padded to a multiple of 32 floats, each region
+ * 256-byte aligned.  Returns 0 for invalid sizes.
  */
 size_t sparstar_score_workspace_bytes(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size);
 

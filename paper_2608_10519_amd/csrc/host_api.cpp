@@ -183,10 +183,13 @@ extern "C" int sparstar_scale_densities(const int64_t* scale_lq, int n_scales, c
 extern "C" const char* sparstar_last_error(void) { return g_error.c_str(); }
 
 // Selector workspace: the pooled blocks split into fp16 hi and lo parts (4 D
-// bytes per block), their power-of-two scales, then S.
+// bytes per block), their power-of-two scales, then S with its rows padded to
+// whole 128-byte lines (an S passed in by the caller keeps rows of n_k).
 struct WsLayout {
   size_t q_bar, k_bar, q_exp, k_exp, s, total;
 };
+
+static int64_t s_row_stride(int64_t nk) { return (nk + 31) / 32 * 32; }
 
 static WsLayout ws_layout(int B, int H, int64_t Lq, int64_t Lk, int D, int block_size) {
   const int64_t bh = int64_t(B) * H;
@@ -197,7 +200,7 @@ static WsLayout ws_layout(int B, int H, int64_t Lq, int64_t Lk, int D, int block
   w.q_exp = w.k_bar + align256(size_t(bh * nk * D) * 4);
   w.k_exp = w.q_exp + align256(size_t(bh * nq) * sizeof(int32_t));
   w.s = w.k_exp + align256(size_t(bh * nk) * sizeof(int32_t));
-  w.total = w.s + align256(size_t(bh * nq * nk) * sizeof(float));
+  w.total = w.s + align256(size_t(bh * nq * s_row_stride(nk)) * sizeof(float));
   return w;
 }
 
@@ -254,6 +257,7 @@ static int score_common(const void* q, const void* k, int B, int H, int64_t Lq, 
   int32_t* q_exp = reinterpret_cast<int32_t*>(ws + wl.q_exp);
   int32_t* k_exp = reinterpret_cast<int32_t*>(ws + wl.k_exp);
   float* s = scores ? scores : reinterpret_cast<float*>(ws + wl.s);
+  const int s_stride = int(scores ? nk : s_row_stride(nk));
   hipStream_t st = static_cast<hipStream_t>(stream);
 
   PoolArgs pa{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), q_bar, k_bar, q_exp, k_exp, Lq, Lk,
@@ -264,17 +268,18 @@ static int score_common(const void* q, const void* k, int B, int H, int64_t Lq, 
   if (fused) {
     // scores and selection in one kernel, S kept in LDS
     ScoreSelectArgs fa{q_bar, k_bar, q_exp, k_exp, kv_num_blocks, kv_indices, bh, int(nq), int(nk), H, kv_stride, D,
-                       tau, kb, hb};
+                       int(n_sel), tau, kb, hb};
     e = launch_score_select(fa, st);
     if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "score/select launch: %s", hipGetErrorString(e));
     return ok();
   }
   if (n_sel > 0) {
-    ScoreArgs sa{q_bar, k_bar, q_exp, k_exp, s, bh, int(nq), int(nk), tau, kb};
+    ScoreArgs sa{q_bar, k_bar, q_exp, k_exp, s, bh, int(nq), int(nk), s_stride, tau, kb};
     e = launch_score(sa, D, st);
     if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "score launch: %s", hipGetErrorString(e));
   }
-  SelectArgs sel{s, kv_num_blocks, kv_indices, int64_t(bh) * nq, int(nq), int(nk), H, kv_stride, kb, hb};
+  SelectArgs sel{s, kv_num_blocks, kv_indices, int64_t(bh) * nq, int(nq), int(nk), H, kv_stride, int(n_sel),
+                 s_stride, kb, hb};
   e = launch_select(sel, st);
   if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "select launch: %s", hipGetErrorString(e));
   return ok();

@@ -45,18 +45,21 @@ struct ScoreArgs {
   const uint16_t* k_bar;  // [BH, n_k, 2 D] fp16 (hi, lo)
   const int32_t* q_exp;   // [BH, n_q]
   const int32_t* k_exp;   // [BH, n_k]
-  float* s;               // [BH, n_q, n_k]
+  float* s;               // [BH, n_q, s_stride]
   int bh, n_q, n_k;
+  int s_stride;           // floats per row of S (>= n_k)
   float tau;           // D^-1/2
   KeepBlocks keep;
 };
 
 struct SelectArgs {
-  const float* s;          // [BH, n_q, n_k]
+  const float* s;          // [BH, n_q, s_stride]
   int32_t* kv_num_blocks;  // [BH, n_q]
   int32_t* kv_indices;     // [BH, n_q, stride]
   int64_t rows;            // BH * n_q
   int n_q, n_k, heads, stride;
+  int n_sel;               // selectable key blocks per row (Eq. 4)
+  int s_stride;            // floats per row of S (>= n_k)
   KeepBlocks keep;
   HeadBudgets budget;
 };
@@ -75,6 +78,7 @@ struct ScoreSelectArgs {
   int32_t* kv_num_blocks;  // [BH, n_q]
   int32_t* kv_indices;     // [BH, n_q, stride]
   int bh, n_q, n_k, heads, stride, d;
+  int n_sel;               // selectable key blocks per row (Eq. 4)
   float tau;               // D^-1/2
   KeepBlocks keep;
   HeadBudgets budget;

@@ -98,12 +98,13 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
 
 // ---------------------------------------------------------------------------
 // score: one work-group per (bh, 64 query blocks, 64 key blocks) tile of S,
-// four waves, each a 32 x 32 sub-tile on v_mfma_f32_32x32x16_f16.  D is
-// streamed through LDS in chunks of SKC columns (16-byte loads of the hi and
-// lo parts), each LDS row holding the chunk's hi then lo values of one pooled
-// row, padded to 144 bytes: 16 consecutive rows read at one 16-byte offset
-// then fall on 16 disjoint groups of four banks.  The next chunk's loads are
-// in flight while the current chunk is multiplied.
+// four waves, each a 32 x 32 sub-tile on v_mfma_f32_32x32x16_f16.  Every
+// thread issues all of its global loads (its row's 16-byte pieces of the hi and
+// lo parts, for all of D) at once, so a work-group waits for memory once; D
+// then goes through LDS in chunks of SKC columns, each LDS row holding the
+// chunk's hi then lo values of one pooled row, padded to 144 bytes: 16
+// consecutive rows read at one 16-byte offset then fall on 16 disjoint groups
+// of four banks.
 //
 // MFMA operands (lane l, h = l / 32): A[m][k] = qbar[m = l % 32][d],
 // B[k][n] = kbar[n = l % 32][d], k = 8 h + i over the lane's 8 fp16 values at
@@ -121,7 +122,9 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   __shared__ int qe[ST], ke[ST];
   const int tiles_i = (a.n_q + ST - 1) / ST;
   const int tiles_j = (a.n_k + ST - 1) / ST;
-  int64_t wg = blockIdx.x;
+  // consecutive tiles (one head's, key tiles fastest) on the same XCD, whose
+  // L2 then holds that head's pooled blocks
+  int64_t wg = xcd_linear(blockIdx.x, (int64_t)gridDim.x);
   const int tj = (int)(wg % tiles_j);
   wg /= tiles_j;
   const int ti = (int)(wg % tiles_i);
@@ -142,7 +145,15 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   auto keep_if = [](bool ok, uint4 v) {
     return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
   };
-  uint4 qh = ld(qrow), ql = ld(qrow + D), kh = ld(krow), kl = ld(krow + D);
+  constexpr int NC = D / SKC;
+  uint4 qh[NC], ql[NC], kh[NC], kl[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    qh[c] = ld(qrow + c * SKC);
+    ql[c] = ld(qrow + D + c * SKC);
+    kh[c] = ld(krow + c * SKC);
+    kl[c] = ld(krow + D + c * SKC);
+  }
   if (t < ST) qe[t] = i0 + t < a.n_q ? a.q_exp[bh * a.n_q + i0 + t] : 0;
   else if (t < 2 * ST) ke[t - ST] = j0 + t - ST < a.n_k ? a.k_exp[bh * a.n_k + j0 + t - ST] : 0;
 
@@ -150,19 +161,13 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.f;
 #pragma unroll
-  for (int d0 = 0; d0 < D; d0 += SKC) {
-    if (d0 > 0) __syncthreads();  // the previous chunk's reads are done
-    *reinterpret_cast<uint4*>(qs + lr * RB + 16 * lc) = keep_if(q_ok, qh);
-    *reinterpret_cast<uint4*>(qs + lr * RB + 64 + 16 * lc) = keep_if(q_ok, ql);
-    *reinterpret_cast<uint4*>(ks + lr * RB + 16 * lc) = keep_if(k_ok, kh);
-    *reinterpret_cast<uint4*>(ks + lr * RB + 64 + 16 * lc) = keep_if(k_ok, kl);
+  for (int c = 0; c < NC; ++c) {
+    if (c > 0) __syncthreads();  // the previous chunk's reads are done
+    *reinterpret_cast<uint4*>(qs + lr * RB + 16 * lc) = keep_if(q_ok, qh[c]);
+    *reinterpret_cast<uint4*>(qs + lr * RB + 64 + 16 * lc) = keep_if(q_ok, ql[c]);
+    *reinterpret_cast<uint4*>(ks + lr * RB + 16 * lc) = keep_if(k_ok, kh[c]);
+    *reinterpret_cast<uint4*>(ks + lr * RB + 64 + 16 * lc) = keep_if(k_ok, kl[c]);
     __syncthreads();
-    if (d0 + SKC < D) {
-      qh = ld(qrow + d0 + SKC);
-      ql = ld(qrow + D + d0 + SKC);
-      kh = ld(krow + d0 + SKC);
-      kl = ld(krow + D + d0 + SKC);
-    }
     const unsigned char* qa = qs + (wq * 32 + l32) * RB + 16 * h;
     const unsigned char* kc = ks + (wk * 32 + l32) * RB + 16 * h;
 #pragma unroll
@@ -180,12 +185,12 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   const int j = j0 + wk * 32 + l32;
   if (j >= a.n_k || keep_block(a.keep, j)) return;  // no barrier below
   const int ej = ke[wk * 32 + l32];
-  float* scol = a.s + bh * (int64_t)a.n_q * a.n_k + j;
+  float* scol = a.s + bh * (int64_t)a.n_q * a.s_stride + j;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     const int r = wq * 32 + 8 * (e / 4) + 4 * h + (e % 4);
     const int i = i0 + r;
-    if (i < a.n_q) scol[(int64_t)i * a.n_k] = a.tau * __builtin_amdgcn_ldexpf(acc[e], qe[r] + ej);
+    if (i < a.n_q) scol[(int64_t)i * a.s_stride] = a.tau * __builtin_amdgcn_ldexpf(acc[e], qe[r] + ej);
   }
 }
 

@@ -27,6 +27,12 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// The same key from the float's bits.
+__device__ __forceinline__ uint32_t order_key_bits(uint32_t u) {
+  u = u == 0x80000000u ? 0u : u;
+  return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+}
+
 __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
@@ -39,7 +45,7 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_kernel(SelectArgs a) {
   const int64_t r = live ? row : 0;
   const int h = (int)((r / a.n_q) % a.heads);
   const int kk = a.budget.k[h];
-  const float* s = a.s + r * a.n_k;
+  const float* s = a.s + r * a.s_stride;
   const int chunks = (a.n_k + 63) / 64;
 
   uint32_t prefix = 0, mask = 0;
@@ -116,89 +122,215 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_kernel(SelectArgs a) {
 // Forced blocks and blocks past n_k hold key 0, below every real key (the
 // smallest order key of a non-NaN float is 0x007fffff), so they never count.
 //
-// Selection of one row whose keys sit in registers: key[c] of lane L is the key
-// of block 64 c + L.  Every lane of the wave calls it.
+// The keys of a row sit in registers: key[c] of lane L is the key of block
+// 64 c + L.  Every helper below is called by every lane of the wave.
+
+// Number of keys >= x (wave-uniform).
 template <int C>
-__device__ __forceinline__ void select_row_regs(const uint32_t (&key)[C], int n_k, int kk, const KeepBlocks& keep,
-                                                int lane, int32_t* out, int32_t* num_out) {
-  // thr, take_ties: take every candidate with key > thr and the first
-  // take_ties candidates (in block order) with key == thr
-  uint32_t thr = 0xffffffffu, take_ties = 0;  // kk == 0: nothing selectable
-  if (kk > 0) {
-    uint32_t t = 0;
-    bool exact = false;
-    for (int b = 31; b >= 0; --b) {
-      const uint32_t tt = t | (1u << b);
-      int n = 0;
+__device__ __forceinline__ int count_ge(const uint32_t (&key)[C], uint32_t x) {
+  int n = 0;
 #pragma unroll
-      for (int c = 0; c < C; ++c) n += __builtin_popcountll(__ballot(key[c] >= tt));
-      if (n >= kk) {
-        t = tt;
-        if (n == kk) {
-          exact = true;
-          break;
-        }
+  for (int c = 0; c < C; ++c) n += __builtin_popcountll(__ballot(key[c] >= x));
+  return n;
+}
+
+// Top-down bit search: from t (bits above b0 already fixed, count_ge(t) >= kk),
+// the largest t with count_ge(t) >= kk, decided one bit at a time.  It stops
+// early when some t has exactly kk keys >= t, and then sets `exact`.
+template <int C>
+__device__ __forceinline__ uint32_t bit_search(const uint32_t (&key)[C], int kk, uint32_t t, int b0, bool& exact) {
+  exact = false;
+  for (int b = b0; b >= 0; --b) {
+    const uint32_t tt = t | (1u << b);
+    const int n = count_ge<C>(key, tt);
+    if (n >= kk) {
+      t = tt;
+      if (n == kk) {
+        exact = true;
+        break;
       }
-    }
-    // t >= 1 here: the kk <= n_sel real keys are all >= 1
-    if (exact) {
-      thr = t - 1;  // the keys >= t are exactly the kk largest
-    } else {
-      // t is the kk-th largest key; the keys above it are all taken
-      int n_gt = 0;
-      if (t != 0xffffffffu) {
-#pragma unroll
-        for (int c = 0; c < C; ++c) n_gt += __builtin_popcountll(__ballot(key[c] > t));
-      }
-      thr = t;
-      take_ties = (uint32_t)(kk - n_gt);
     }
   }
-  int pos = 0;
-  uint32_t ties = 0;
+  return t;
+}
+
+// The selection rule of a row: take every candidate key > thr and the first
+// take_ties candidates (in block order) whose key equals thr.
+struct SelRule {
+  uint32_t thr, take_ties;
+};
+
+// The rule for the kk largest keys (1 <= kk <= number of real keys) by a bit
+// search over the whole row.
+template <int C>
+__device__ __forceinline__ SelRule rule_full(const uint32_t (&key)[C], int kk) {
+  bool exact;
+  const uint32_t t = bit_search<C>(key, kk, 0u, 31, exact);
+  if (exact) return {t - 1, 0u};  // the keys >= t are exactly the kk largest
+  // t is the kk-th largest key (>= 1); the keys above it are all taken
+  const int n_gt = t != 0xffffffffu ? count_ge<C>(key, t + 1) : 0;
+  return {t, (uint32_t)(kk - n_gt)};
+}
+
+// Candidate keys per lane for the bracketed search (1024 per row).
+constexpr int kSelCand = 16;
+
+template <int M>
+__device__ __forceinline__ SelRule rule_from_candidates(const uint32_t* buf, int m, int lane, int kk, int g_hi,
+                                                        uint32_t t_lo, uint32_t upper) {
+  uint32_t cand[M];
 #pragma unroll
-  for (int c = 0; c < C; ++c) {
-    if (64 * c >= n_k) break;
-    const int j = 64 * c + lane;
-    const bool valid = j < n_k;
-    const bool forced = valid && keep_block(keep, j);
-    const bool cand = valid && !forced;
-    const bool tie = cand && key[c] == thr;
-    const uint64_t tie_mask = __ballot(tie);
-    const uint32_t tie_rank = ties + (uint32_t)lanes_below(tie_mask);
-    const bool take = forced || (cand && (key[c] > thr || (tie && tie_rank < take_ties)));
-    const uint64_t take_mask = __ballot(take);
-    if (take) out[pos + lanes_below(take_mask)] = j;
-    pos += __popcll(take_mask);
-    ties += (uint32_t)__popcll(tie_mask);
+  for (int i = 0; i < M; ++i) cand[i] = 64 * i + lane < m ? buf[64 * i + lane] : 0u;
+  // the kc-th largest candidate is the kk-th largest key
+  const int kc = kk - g_hi;
+  const uint32_t diff = t_lo ^ upper;  // the range shares the bits above b0
+  const int b0 = diff == 0 ? -1 : 31 - __builtin_clz(diff);
+  const uint32_t t0 = b0 == 31 ? 0u : (b0 < 0 ? t_lo : (t_lo & ~((2u << b0) - 1u)));
+  bool exact;
+  uint32_t t = bit_search<M>(cand, kc, t0, b0, exact);
+  if (exact) {
+    // exactly kc candidates are >= t; below t_lo that also counts keys outside
+    // the range, so the rule starts at t_lo at the lowest
+    t = t < t_lo ? t_lo : t;
+    return {t - 1, 0u};
+  }
+  const int n_gt = g_hi + (t != 0xffffffffu ? count_ge<M>(cand, t + 1) : 0);
+  return {t, (uint32_t)(kk - n_gt)};
+}
+
+// The rule for the kk largest keys, bracketed from a sample first.  samp[] holds
+// the keys of 128 evenly spaced blocks of the row (samp[0] of lane L: sample L,
+// samp[1]: sample 64 + L; 0 for forced ones).  The sample ranks around the
+// expected rank of the kk-th key (a margin of about 2.2 standard deviations of
+// the binomial count) give thresholds t_lo <= t_hi; two counts over the row
+// check that the kk-th key lies in [t_lo, t_hi), and the keys there (a few
+// hundred) are compacted through the wave's LDS buffer `buf` (64 kSelCand
+// words) and searched alone.  When the bracket misses or holds too many keys,
+// the whole row is searched.
+template <int C>
+__device__ __forceinline__ SelRule rule_sampled(const uint32_t (&key)[C], int kk, int n_sel, const uint32_t (&samp)[2],
+                                                uint32_t* buf, int lane) {
+  const int s_real = count_ge<2>(samp, 1u);
+  if (s_real >= 16 && n_sel > 0 && kk < n_sel) {
+    const float p = (float)kk / (float)n_sel;
+    const float mid = p * (float)s_real;  // expected number of sampled keys >= the kk-th key
+    const int margin = (int)(2.2f * sqrtf((float)s_real * p * (1.f - p))) + 2;
+    const int r1 = (int)mid - margin, r2 = (int)mid + 1 + margin;
+    bool ex;
+    const bool has_hi = r1 >= 1;
+    const uint32_t t_hi = has_hi ? bit_search<2>(samp, r1, 0u, 31, ex) : 0u;
+    const uint32_t t_lo = r2 <= s_real ? bit_search<2>(samp, r2, 0u, 31, ex) : 1u;
+    const int g_hi = has_hi ? count_ge<C>(key, t_hi) : 0;  // keys above the range
+    const int g_lo = count_ge<C>(key, t_lo);
+    const int m = g_lo - g_hi;                             // keys in [t_lo, t_hi)
+    if (g_hi < kk && kk <= g_lo && m <= 64 * kSelCand) {
+      int base = 0;
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        const bool in = key[c] >= t_lo && (!has_hi || key[c] < t_hi);
+        const uint64_t mask = __ballot(in);
+        if (in) buf[base + lanes_below(mask)] = key[c];
+        base += __popcll(mask);
+      }
+      const uint32_t upper = has_hi ? t_hi - 1 : 0xffffffffu;
+      if (m <= 64 * 4) return rule_from_candidates<4>(buf, m, lane, kk, g_hi, t_lo, upper);
+      if (m <= 64 * 8) return rule_from_candidates<8>(buf, m, lane, kk, g_hi, t_lo, upper);
+      return rule_from_candidates<kSelCand>(buf, m, lane, kk, g_hi, t_lo, upper);
+    }
+  }
+  return rule_full<C>(key, kk);
+}
+
+// Writes the row's list: the forced blocks and the selected ones, ascending.
+// A block is forced when it lies below n_k and holds key 0 (real keys are
+// >= 0x007fffff).  Without ties to break (take_ties == 0, the usual case) a
+// block is taken when forced or above thr.
+template <int C>
+__device__ __forceinline__ void emit_row(const uint32_t (&key)[C], int n_k, SelRule rule, int lane, int32_t* out,
+                                         int32_t* num_out) {
+  int pos = 0;
+  if (rule.take_ties == 0) {
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      if (64 * c >= n_k) break;
+      const bool valid = 64 * c + 64 <= n_k || 64 * c + lane < n_k;
+      const bool take = key[c] > rule.thr || (key[c] == 0u && valid);
+      const uint64_t take_mask = __ballot(take);
+      if (take) out[pos + lanes_below(take_mask)] = 64 * c + lane;
+      pos += __popcll(take_mask);
+    }
+  } else {
+    uint32_t ties = 0;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      if (64 * c >= n_k) break;
+      const bool valid = 64 * c + 64 <= n_k || 64 * c + lane < n_k;
+      const bool tie = key[c] == rule.thr;  // thr >= 1: never a forced block
+      const uint64_t tie_mask = __ballot(tie);
+      const uint32_t tie_rank = ties + (uint32_t)lanes_below(tie_mask);
+      const bool take = key[c] > rule.thr || (tie && tie_rank < rule.take_ties) || (key[c] == 0u && valid);
+      const uint64_t take_mask = __ballot(take);
+      if (take) out[pos + lanes_below(take_mask)] = 64 * c + lane;
+      pos += __popcll(take_mask);
+      ties += (uint32_t)__popcll(tie_mask);
+    }
   }
   if (lane == 0) *num_out = pos;
 }
 
+// Bit c of lane L: whether block 64 c + L (c < 64) is forced.
+__device__ __forceinline__ uint64_t forced_mask(const KeepBlocks& kb, int lane) {
+  auto below = [](int x) -> uint64_t {  // bits [0, x)
+    return x <= 0 ? 0ull : (x >= 64 ? ~0ull : (1ull << x) - 1ull);
+  };
+  uint64_t m = 0;
+#pragma unroll
+  for (int t = 0; t < kMaxKeep; ++t) {
+    if (t >= kb.n) break;  // uniform: a kernel argument
+    // the chunks c with begin <= 64 c + lane < end
+    const int c_lo = kb.begin[t] <= lane ? 0 : (kb.begin[t] - lane + 63) / 64;
+    const int c_hi = kb.end[t] <= lane ? 0 : (kb.end[t] - lane + 63) / 64;
+    m |= below(c_hi) & ~below(c_lo);
+  }
+  return m;
+}
+
+// Sample i (0..127) of a row of n_k blocks: the middle block of the i-th of 128
+// equal segments.
+__device__ __forceinline__ int sample_block(int i, int n_k) { return (int)(((2 * (int64_t)i + 1) * n_k) / 256); }
+
 // Rows of up to 64 C blocks: one wave per row reads its row of S straight
-// into registers (coalesced, 256 bytes per load).
+// into registers (coalesced, 256 bytes per load) through one buffer
+// descriptor, so that loads past n_k need no clamp (they read 0).
 template <int C>
 __global__ __launch_bounds__(64 * kSelWaves) void select_reg_kernel(SelectArgs a) {
-  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  __shared__ uint32_t cbuf[kSelWaves][64 * kSelCand];
+  // the wave index as a scalar, so that the row's descriptor is one too
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64), lane = threadIdx.x % 64;
   const int64_t row = (int64_t)blockIdx.x * kSelWaves + wave;
   if (row >= a.rows) return;  // wave-uniform; no barrier below
   const int h = (int)((row / a.n_q) % a.heads);
-  const float* s = a.s + row * a.n_k;
-  // all loads first (in bounds, independent), then the keys
-  float sv[C];
-#pragma unroll
-  for (int c = 0; c < C; ++c) {
-    const int j = 64 * c + lane;
-    sv[c] = s[j < a.n_k ? j : a.n_k - 1];
-  }
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.s + row * a.s_stride), (short)0, a.n_k * 4, 0x00020000);
+  // all loads first (independent), then the keys in place
   uint32_t key[C];
 #pragma unroll
+  for (int c = 0; c < C; ++c) key[c] = __builtin_amdgcn_raw_buffer_load_b32(rs, (64 * c + lane) * 4, 0, 0);
+  const int b0 = sample_block(lane, a.n_k), b1 = sample_block(64 + lane, a.n_k);
+  const uint32_t sp0 = __builtin_amdgcn_raw_buffer_load_b32(rs, b0 * 4, 0, 0);
+  const uint32_t sp1 = __builtin_amdgcn_raw_buffer_load_b32(rs, b1 * 4, 0, 0);
+  const uint64_t fm = forced_mask(a.keep, lane);
+#pragma unroll
   for (int c = 0; c < C; ++c) {
-    const int j = 64 * c + lane;
-    key[c] = (j < a.n_k && !keep_block(a.keep, j)) ? order_key(sv[c]) : 0u;
+    const bool real = (64 * c + 64 <= a.n_k || 64 * c + lane < a.n_k) && !((fm >> c) & 1ull);
+    key[c] = real ? order_key_bits(key[c]) : 0u;
   }
-  select_row_regs<C>(key, a.n_k, a.budget.k[h], a.keep, lane, a.kv_indices + row * a.stride,
-                     a.kv_num_blocks + row);
+  const uint32_t samp[2] = {keep_block(a.keep, b0) ? 0u : order_key_bits(sp0),
+                            keep_block(a.keep, b1) ? 0u : order_key_bits(sp1)};
+  const int kk = a.budget.k[h];
+  // kk == 0: nothing selectable
+  const SelRule rule = kk > 0 ? rule_sampled<C>(key, kk, a.n_sel, samp, cbuf[wave], lane) : SelRule{0xffffffffu, 0u};
+  emit_row<C>(key, a.n_k, rule, lane, a.kv_indices + row * a.stride, a.kv_num_blocks + row);
 }
 
 // ---------------------------------------------------------------------------
@@ -297,7 +429,7 @@ __global__ __launch_bounds__(64 * kFusedRows) void score_select_kernel(ScoreSele
 
   const int i = i0 + wave;
   if (i >= a.n_q) return;  // wave-uniform; no barrier below
-  const uint32_t* rk = fused_keys + (size_t)wave * row_len;
+  uint32_t* rk = fused_keys + (size_t)wave * row_len;
   uint32_t key[C];
 #pragma unroll
   for (int c = 0; c < C; ++c) {
@@ -305,9 +437,13 @@ __global__ __launch_bounds__(64 * kFusedRows) void score_select_kernel(ScoreSele
     const uint32_t v = rk[j < row_len ? j : row_len - 1];  // in bounds, independent reads
     key[c] = j < a.n_k ? v : 0u;
   }
+  const uint32_t samp[2] = {rk[sample_block(lane, a.n_k)], rk[sample_block(64 + lane, a.n_k)]};
   const int64_t r = bh * a.n_q + i;
-  select_row_regs<C>(key, a.n_k, a.budget.k[(int)(bh % a.heads)], a.keep, lane, a.kv_indices + r * a.stride,
-                     a.kv_num_blocks + r);
+  const int kk = a.budget.k[(int)(bh % a.heads)];
+  // the row's own LDS keys are in registers now: their space holds the
+  // bracketed candidates (at most min(n_k, 64 kSelCand) of them)
+  const SelRule rule = kk > 0 ? rule_sampled<C>(key, kk, a.n_sel, samp, rk, lane) : SelRule{0xffffffffu, 0u};
+  emit_row<C>(key, a.n_k, rule, lane, a.kv_indices + r * a.stride, a.kv_num_blocks + r);
 }
 
 size_t score_select_lds_bytes(int n_k) { return (size_t)kFusedRows * ((n_k + 15) / 16 * 16) * sizeof(uint32_t); }

@@ -39,10 +39,11 @@ def test_exports_every_declared_symbol(lib):
 
 def test_workspace_bytes(lib):
     # 720p: qbar 24*1125*128*4, kbar 24*2258*128*4, their scales 24*1125*4 and
-    # 24*2258*4, S 24*1125*2258*4 (256-aligned regions)
+    # 24*2258*4, S 24*1125*2272*4 (rows of 2258 floats padded to 2272;
+    # 256-aligned regions)
     al = lambda x: (x + 255) // 256 * 256
     want = (al(24 * 1125 * 128 * 4) + al(24 * 2258 * 128 * 4) + al(24 * 1125 * 4) + al(24 * 2258 * 4)
-            + al(24 * 1125 * 2258 * 4))
+            + al(24 * 1125 * 2272 * 4))
     assert S.sparstar_score_workspace_bytes(1, 24, 72_000, 144_512, 128, 64) == want
     assert S.sparstar_score_workspace_bytes(1, 24, 72_000, 144_512, 96, 64) == 0
     assert S.sparstar_score_workspace_bytes(0, 24, 72_000, 144_512, 128, 64) == 0
@@ -149,7 +150,7 @@ def _score_static(lib, **over):
     (dict(keep=[(0, 2000)]), S.ERR_INVALID_ARG, "keep[0]"),
     (dict(stride=5), S.ERR_INVALID_ARG, "kv_stride"),
     (dict(scores=FAKE + 2), S.ERR_INVALID_ARG, "scores"),
-    # the 720p shape (24 heads, 72,000 queries, 144,512 keys, D 128): qbar + kbar + S = 285 MB
+    # the 720p shape (24 heads, 72,000 queries, 144,512 keys, D 128): qbar + kbar, scales and S = 287 MB
     (dict(H=24, Lq=72_000, Lk=144_512, D=128, keep=[(72_000, 72_512)], stride=571), S.ERR_WORKSPACE,
      "more than the 67108864 bytes"),
 ])
@@ -162,7 +163,8 @@ def test_score_blocks_static_rejects_before_any_hip_call(lib, over, code, msg):
 
 def test_score_blocks_static_scratch_limit():
     """With `scores` given, S stays out of the static scratch: at the 720p shape
-    qbar + kbar (41.6 MB) fit, which the next check (a too-small stride) shows."""
+    qbar + kbar and their scales (41.9 MB) fit, which the next check (a too-small
+    stride) shows."""
     lib = S.load()
     big = dict(H=24, Lq=72_000, Lk=144_512, D=128, keep=[(72_000, 72_512)])
     assert _score_static(lib, **big, stride=5, scores=FAKE) == S.ERR_INVALID_ARG

@@ -42,7 +42,8 @@ def _ws_views(ws, B, H, n_q, n_k, D):
     def decode(off, rows, off_e, n):
         hl = raw[off: off + rows * D * 4].view(np.float16).reshape(rows, 2, D).astype(np.float64)
         e = raw[off_e: off_e + rows * 4].view(np.int32).astype(np.float64)
-        return ((hl[:, 0] + hl[:, 1]) * np.exp2(e)[:, None]).reshape(B, H, n, D)
+        with np.errstate(all="ignore"):  # forced key blocks are never pooled: their rows hold anything
+            return ((hl[:, 0] + hl[:, 1]) * np.exp2(e)[:, None]).reshape(B, H, n, D)
 
     return decode(0, rq, off_qe, n_q), decode(off_k, rk, off_ke, n_k)
 
