@@ -276,6 +276,47 @@ def test_selector_ties_prefer_lower_index(gpu_lib):
         assert len(row) == len(keep_set) + 3
 
 
+@pytest.mark.parametrize("n_distinct", [1, 40])
+def test_selector_heavy_ties_in_long_rows(gpu_lib, n_distinct):
+    """Rows of 2,270 key blocks whose selectable blocks are copies of only
+    n_distinct blocks: every row's scores take at most n_distinct values, the
+    k-th largest sits inside a tied group of dozens of blocks (or of all of
+    them), and the sampled bracket of the register search sees repeated keys.
+    The lowest indices of the tied group must be taken, on the GPU's own fp32
+    scores (separate kernels) and among the copies (fused kernel)."""
+    w = TINY.with_(name=f"heavy-ties-{n_distinct}", heads=1, lq=64 * 6, l_ref=64 * 2270 - 64 * 6 - 128,
+                   l_text=128, seed=16)
+    qb_, kb_, _ = generate(w)
+    kb_ = kb_.copy()
+    blk, n_k = w.block, -(-w.lk // w.block)
+    assert n_k <= gpu_lib.FUSED_MAX_BLOCKS
+    src = [37 + 17 * i for i in range(n_distinct)]
+    orig = kb_.copy()  # copy from the original blocks: a source block is itself a member of another group
+    for j in range(n_k):
+        s0 = src[j % n_distinct]
+        if (j + 1) * blk <= w.lk:
+            kb_[0, 0, j * blk:(j + 1) * blk] = orig[0, 0, s0 * blk:(s0 + 1) * blk]
+    keep, keep_ref = keep_for(gpu_lib, w)
+    keep_set = O.keep_blocks(keep_ref, w.lk, w.block)
+    sel = O.selectable_blocks(keep_set, w.lk, w.block)
+    kk = O.budget_k(w.density, len(sel))
+    num, idx, scores, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, w.density)
+    s = scores.cpu().numpy()[0, 0]
+    for i, row in enumerate(lists_from_device(num, idx)[0][0]):
+        want = sorted(set(keep_set) | set(O.topk_idx(s[i].astype(np.float64), sel, kk)))
+        assert row == want, (i, len(row), len(want))
+    num_f, idx_f, _, _, _ = _run_selector(gpu_lib, w, to_dev(qb_), to_dev(kb_), keep, w.density,
+                                          with_scores=False, fused=True)
+    groups = {}
+    for j in sel:
+        groups.setdefault(j % n_distinct if (j + 1) * blk <= w.lk else -1 - j, []).append(j)
+    for i, row in enumerate(lists_from_device(num_f, idx_f)[0][0]):
+        assert len(row) == len(keep_set) + kk
+        for g in groups.values():
+            taken = [j for j in row if j in g]
+            assert taken == g[: len(taken)], (i, taken[:5], g[:5])
+
+
 def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_override=None, split=True,
                k_override=None):
     """Run the sparse forward with given lists on all heads; return GPU and oracle outputs."""
