@@ -173,9 +173,14 @@ int sparstar_score_blocks_fused(const void* q, const void* k, int B, int H, int6
 
 /*
  * Bytes of device workspace that lets the attention calls below split the key
- * blocks of every query block into 16 contiguous ranges (two per XCD of the
- * MI355X, taken one after the other, so that each XCD's L2 streams about one
- * sixteenth of a head's K/V at a time) and merge the partial results: per
+ * blocks of every query block into contiguous ranges and merge the partial
+ * results.  Lists that can hold >= 24,576 keys (kv_stride x block_size; for
+ * the dense call, every key block of the row) take 16 ranges (two per XCD of
+ * the MI355X, taken one after the other, so that each XCD's L2 streams about
+ * one sixteenth of a head's K/V at a time); shorter lists take 8, one per XCD,
+ * where the fixed cost of each range outweighs the locality.  So the dense call
+ * and a sparse call whose lists name every block, in order, give the same bits.
+ * The workspace is sized for 16: per
  * (batch, head, query block, range, query row) the range's unnormalised
  * partial P V in fp16, scaled by a power of two chosen per row so that its
  * largest magnitude lies in [0.5, 1) ([.., D]; any finite bf16 range of V keeps

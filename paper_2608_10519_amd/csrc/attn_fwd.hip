@@ -198,13 +198,13 @@ void attn_fwd_kernel(AttnArgs a) {
 
   // Work item.  Work-groups are dispatched round-robin over the eight XCDs, so
   // with the key-range split the work-group id decodes as
-  //   id = ((bh * S + s) * n_q + qb) * 8 + x,  range r = 8 s + x,  S = kSplits / 8:
+  //   id = ((bh * S + s) * n_q + qb) * 8 + x,  range r = 8 s + x,  S = n_splits / 8:
   // XCD x runs range x of every query block of head bh, then range 8 + x, ...,
   // and its L2 holds one range of the head's K/V at a time.
   int split = 0;
   int64_t work = blockIdx.x;
   if constexpr (SPLIT) {
-    constexpr int S = kSplits / 8;
+    const int S = a.n_splits / 8;
     const int64_t x = blockIdx.x % 8, rest = blockIdx.x / 8;
     const int64_t qbi = rest % a.n_q, rest2 = rest / a.n_q;
     split = (int)((rest2 % S) * 8 + x);
@@ -212,8 +212,8 @@ void attn_fwd_kernel(AttnArgs a) {
   }
   const int64_t bh = work / a.n_q;
   const int qb = (int)(work % a.n_q);
-  const int blk_lo = SPLIT ? (int)((int64_t)split * a.n_k / kSplits) : 0;
-  const int blk_hi = SPLIT ? (int)((int64_t)(split + 1) * a.n_k / kSplits) : a.n_k;
+  const int blk_lo = SPLIT ? (int)((int64_t)split * a.n_k / a.n_splits) : 0;
+  const int blk_hi = SPLIT ? (int)((int64_t)(split + 1) * a.n_k / a.n_splits) : a.n_k;
 
   const int tid = threadIdx.x, lane = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
@@ -684,7 +684,7 @@ void attn_fwd_kernel(AttnArgs a) {
     ex = ex < -126 ? -126 : ex;
     const float sc = __builtin_amdgcn_ldexpf(1.0f, -ex);
     if (row_ok) {
-      const int64_t prow = (work * kSplits + split) * BLK + qs * 32 + l32o;
+      const int64_t prow = (work * a.n_splits + split) * BLK + qs * 32 + l32o;
       _Float16* po = reinterpret_cast<_Float16*>(a.part_o) + prow * D;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t)
@@ -720,7 +720,7 @@ void attn_fwd_kernel(AttnArgs a) {
   }
 }
 
-// Combines the kSplits partial results of one query block.  Range r left, per
+// Combines the NS partial results of one query block.  Range r left, per
 // query row, A_r = sum of bf16(p) v over its keys scaled by 2^-e_r (fp16), its
 // running max m_r (log2 units), the row sums lb_r (of the bf16 p that multiply
 // V) and le_r (of the fp32 p), and e_r.  With M = max_r m_r and
@@ -739,10 +739,10 @@ struct MergeCfg {
   static_assert(CPT * NT == CHUNKS && NT >= BLK, "chunk split");
 };
 
-template <int D, int BLK>
+template <int D, int BLK, int NS>
 __global__ __launch_bounds__((MergeCfg<D, BLK>::NT)) void attn_merge_kernel(AttnArgs a) {
   using M = MergeCfg<D, BLK>;
-  __shared__ float wts[kSplits][BLK];
+  __shared__ float wts[NS][BLK];
   const int64_t work = blockIdx.x;
   const int64_t bh = work / a.n_q;
   const int qb = (int)(work % a.n_q);
@@ -754,8 +754,8 @@ __global__ __launch_bounds__((MergeCfg<D, BLK>::NT)) void attn_merge_kernel(Attn
     const int row = c / M::CPR, d0 = (c % M::CPR) * 8;
     const int rr = row < rows ? row : 0;
 #pragma unroll
-    for (int r = 0; r < kSplits; ++r) {
-      const int64_t prow = (work * kSplits + r) * BLK + rr;
+    for (int r = 0; r < NS; ++r) {
+      const int64_t prow = (work * NS + r) * BLK + rr;
       v[r] = *reinterpret_cast<const f16x8*>(reinterpret_cast<const _Float16*>(a.part_o) + prow * D + d0);
     }
   };
@@ -764,7 +764,7 @@ __global__ __launch_bounds__((MergeCfg<D, BLK>::NT)) void attn_merge_kernel(Attn
     if (row >= rows) return;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < kSplits; ++r) {
+    for (int r = 0; r < NS; ++r) {
       const float w = wts[r][row];
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc[e] = w != 0.f ? fmaf(w, (float)v[r][e], acc[e]) : acc[e];
@@ -780,23 +780,23 @@ __global__ __launch_bounds__((MergeCfg<D, BLK>::NT)) void attn_merge_kernel(Attn
   // The threads of the first BLK rows turn the per-row records into weights
   // first and then issue their partial loads; every other thread issues its
   // partial loads at once, so that their latency overlaps the records'.
-  f16x8 v[kSplits];
+  f16x8 v[NS];
   if (tid >= BLK) load_chunk(tid, v);
   if (tid < BLK && tid < rows) {
     const int row = tid;
     const float2* rec = reinterpret_cast<const float2*>(a.part_meta);  // record i = float2 pairs 2i, 2i + 1
-    float m[kSplits], lb[kSplits], mm = -INFINITY;
+    float m[NS], lb[NS], mm = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < kSplits; ++r) {
-      const float2 x = rec[2 * ((work * kSplits + r) * BLK + row)];
+    for (int r = 0; r < NS; ++r) {
+      const float2 x = rec[2 * ((work * NS + r) * BLK + row)];
       m[r] = x.x;
       lb[r] = x.y;
       if (lb[r] > 0.f) mm = fmaxf(mm, m[r]);
     }
     float den = 0.f, sum_e = 0.f;
 #pragma unroll
-    for (int r = 0; r < kSplits; ++r) {
-      const float2 y = rec[2 * ((work * kSplits + r) * BLK + row) + 1];  // (le, e)
+    for (int r = 0; r < NS; ++r) {
+      const float2 y = rec[2 * ((work * NS + r) * BLK + row) + 1];  // (le, e)
       const float w = lb[r] > 0.f ? exp2f(m[r] - mm) : 0.f;
       den = fmaf(w, lb[r], den);
       sum_e = fmaf(w, y.x, sum_e);
@@ -804,7 +804,7 @@ __global__ __launch_bounds__((MergeCfg<D, BLK>::NT)) void attn_merge_kernel(Attn
     }
     const float inv = den > 0.f ? 1.f / den : 0.f;
 #pragma unroll
-    for (int r = 0; r < kSplits; ++r) wts[r][row] *= inv;
+    for (int r = 0; r < NS; ++r) wts[r][row] *= inv;
     if (a.lse != nullptr)
       a.lse[bh * a.lq + (int64_t)qb * BLK + row] =
           sum_e > 0.f ? (mm + log2f(sum_e)) * 0.69314718055994530942f : -INFINITY;
@@ -825,11 +825,13 @@ static hipError_t launch_cfg(const AttnArgs& a, bool dense, hipStream_t stream) 
   if (items == 0) return hipSuccess;
   constexpr int NT = AttnCfg<D, BLK>::NT;
   if (a.part_o != nullptr) {
-    if (dense) attn_fwd_kernel<D, BLK, true, true><<<items * kSplits, NT, 0, stream>>>(a);
-    else attn_fwd_kernel<D, BLK, false, true><<<items * kSplits, NT, 0, stream>>>(a);
+    if (a.n_splits != 8 && a.n_splits != kSplits) return hipErrorInvalidValue;
+    if (dense) attn_fwd_kernel<D, BLK, true, true><<<items * a.n_splits, NT, 0, stream>>>(a);
+    else attn_fwd_kernel<D, BLK, false, true><<<items * a.n_splits, NT, 0, stream>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    attn_merge_kernel<D, BLK><<<items, MergeCfg<D, BLK>::NT, 0, stream>>>(a);
+    if (a.n_splits == 8) attn_merge_kernel<D, BLK, 8><<<items, MergeCfg<D, BLK>::NT, 0, stream>>>(a);
+    else attn_merge_kernel<D, BLK, kSplits><<<items, MergeCfg<D, BLK>::NT, 0, stream>>>(a);
   } else {
     if (dense) attn_fwd_kernel<D, BLK, true, false><<<items, NT, 0, stream>>>(a);
     else attn_fwd_kernel<D, BLK, false, false><<<items, NT, 0, stream>>>(a);

@@ -382,6 +382,9 @@ static int attn_common(const void* q, const void* k, const void* v, int B, int H
     char* ws = static_cast<char*>(workspace);
     a.part_o = reinterpret_cast<uint16_t*>(ws);
     a.part_meta = reinterpret_cast<float*>(ws + attn_partial_o_bytes(rows, D));
+    // The dense call lists every key block, so it takes the rule of a full list.
+    const int64_t list_keys = (dense ? nk : int64_t(kv_stride)) * block_size;
+    a.n_splits = list_keys < kFewRangesBelowKeys ? 8 : kSplits;
   }
   hipError_t e = launch_attn(a, D, block_size, dense, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SPARSTAR_ERR_HIP, "attention launch: %s", hipGetErrorString(e));

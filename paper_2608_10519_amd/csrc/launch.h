@@ -96,16 +96,22 @@ struct AttnArgs {
   int bh, n_q, n_k, stride;
   float scale_log2;   // softmax scale * log2(e)
   // Key-range split: with part_o set, work item (bh, query block, r) covers key
-  // blocks [r n_k / kSplits, (r + 1) n_k / kSplits) and writes a partial result
-  // that a merge kernel combines; otherwise one pass writes O and lse.
-  uint16_t* part_o;   // [BH * n_q, kSplits, BLK, D] fp16: the range's unnormalised P V times 2^-e per row
-  float* part_meta;   // [BH * n_q, kSplits, BLK, 4]: running max (log2 units), row sum of the bf16 P,
+  // blocks [r n_k / n_splits, (r + 1) n_k / n_splits) and writes a partial
+  // result that a merge kernel combines; otherwise one pass writes O and lse.
+  uint16_t* part_o;   // [BH * n_q, n_splits, BLK, D] fp16: the range's unnormalised P V times 2^-e per row
+  float* part_meta;   // [BH * n_q, n_splits, BLK, 4]: running max (log2 units), row sum of the bf16 P,
                       // row sum of the fp32 p, e (the row's power-of-two scale, as a float)
+  int n_splits;       // key ranges per query block: 8 or kSplits
 };
 
-// Key ranges per query block: kSplits / 8 consecutive ranges per XCD, so that
-// each XCD's 4 MB L2 holds about one range of a head's K/V at a time.
+// Key ranges per query block: n_splits / 8 consecutive ranges per XCD, so that
+// each XCD's 4 MB L2 holds about one range of a head's K/V at a time.  kSplits
+// is the most (and the workspace is sized for it); short lists take 8 ranges,
+// where the per-range fixed cost (list scan, Q load, epilogue, partial result
+// and its merge) outweighs the L2 locality of the narrower ranges.
 constexpr int kSplits = 16;
+// Lists that can hold fewer keys than this (kv_stride x block size) take 8 ranges.
+constexpr int64_t kFewRangesBelowKeys = 24576;
 
 // Bytes of the fp16 partial-O region of the split workspace (256-byte aligned;
 // the per-row records follow it).

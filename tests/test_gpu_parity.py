@@ -318,8 +318,9 @@ def test_selector_heavy_ties_in_long_rows(gpu_lib, n_distinct):
 
 
 def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_override=None, split=True,
-               k_override=None):
-    """Run the sparse forward with given lists on all heads; return GPU and oracle outputs."""
+               k_override=None, stride=None):
+    """Run the sparse forward with given lists on all heads; return GPU and oracle outputs.
+    stride (default: the longest list) is the kv_stride of the index tensor."""
     import torch
 
     qb_, kb_, vb_ = generate(w)
@@ -331,7 +332,7 @@ def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_ove
         kb_ = k_override(kb_)
     n_q = -(-w.lq // w.block)
     _assert_splits(gpu_lib, w, split)
-    num, idx = lists_to_device([lists_h], n_q)
+    num, idx = lists_to_device([lists_h], n_q, stride)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
     o, lse = gpu_lib.sparstar_sparse_attn_fwd(q, k, v, num, idx, w.block, softmax_scale=scale or 0.0, split=split)
     torch.cuda.synchronize()
@@ -343,9 +344,11 @@ def _attn_case(gpu_lib, w: Workload, lists_h, scale=None, v_override=None, q_ove
     return og, lg, o_ref, l_ref, (qb_, kb_, vb_)
 
 
-# Every case has at least 16 key blocks (the number of key ranges of the split
-# path) and a partial last key block, so the split runs for each of the four
-# (D, b) instances; _attn_case asserts that it does.
+# Every case has at least 16 key blocks (the most key ranges the split path
+# takes) and a partial last key block, so the split runs for each of the four
+# (D, b) instances; _attn_case asserts that it does.  Their lists are short, so
+# they take 8 ranges; test_sixteen_key_ranges_match_oracle widens kv_stride to
+# reach the 16-range launch on the same inputs.
 ATTN_CASES = [
     ("tiny", TINY),
     ("d128-b64-ragged", TINY.with_(name="a1", head_dim=128, lq=500, l_ref=600, l_text=77, heads=3, seed=17)),
@@ -389,6 +392,25 @@ def test_sparse_attention_matches_oracle(gpu_lib, name, w, sharp, split):
     err = check_output(og, o_ref, lg, l_ref, what=name, max_abs=O_MAX_ABS_SHARP if sharp else O_MAX_ABS,
                        lse_abs=LSE_ABS_SHARP if sharp else LSE_ABS)
     _say(f"[attn] {name}: max |dO| = {err:.2e}")
+
+
+# Lists that can hold this many keys (kv_stride x block size) or more take 16
+# key ranges on the split path, shorter ones 8 (include/sparstar.h).
+SIXTEEN_RANGES_FROM_KEYS = 24576
+
+
+@pytest.mark.parametrize("name,w", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
+def test_sixteen_key_ranges_match_oracle(gpu_lib, name, w):
+    """The same lists padded to a kv_stride of 24,576 keys take the 16-range
+    split launch; they must meet the oracle as the 8-range launch does."""
+    rng = np.random.default_rng(zlib.crc32(name.encode()) % 1000 + 11)
+    lists_h = _random_lists(w, rng)
+    stride = -(-SIXTEEN_RANGES_FROM_KEYS // w.block)
+    _say(f"[attn] 16 ranges {name}: kv_stride={stride}")
+    og, lg, o_ref, l_ref, _ = _attn_case(gpu_lib, w, lists_h, stride=stride)
+    check_output(og, o_ref, lg, l_ref, what=name)
+    og8, lg8, _, _, _ = _attn_case(gpu_lib, w, lists_h, stride=stride - 1)
+    check_output(og8, o_ref, lg8, l_ref, what=name + " (8 ranges)")
 
 
 @pytest.mark.parametrize("name,w", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
@@ -448,13 +470,18 @@ def test_dense_attention_matches_oracle(gpu_lib, name, w, split):
                  np.stack([r[1] for r in refs])[None], what=name)
 
 
-@pytest.mark.parametrize("split", [True, False], ids=["split", "onepass"])
-def test_full_lists_equal_dense(gpu_lib, split):
-    """rho = 1 (every block listed) equals the dense forward, bit for bit."""
+@pytest.mark.parametrize("split,long", [(True, False), (True, True), (False, False)],
+                         ids=["split", "split-16-ranges", "onepass"])
+def test_full_lists_equal_dense(gpu_lib, split, long):
+    """rho = 1 (every block listed) equals the dense forward, bit for bit; the
+    long case has 24,576 keys and more, so both calls take 16 key ranges."""
     import torch
 
     w = ATTN_CASES[1][1]
-    _say(f"[dense==sparse(all)] split={split}")
+    if long:
+        w = w.with_(name="a1-long", heads=1, lq=300, l_ref=SIXTEEN_RANGES_FROM_KEYS + 40 - w.l_text - 300)
+        assert w.lk == SIXTEEN_RANGES_FROM_KEYS + 40
+    _say(f"[dense==sparse(all)] split={split} Lk={w.lk}")
     _assert_splits(gpu_lib, w, split)
     qb_, kb_, vb_ = generate(w)
     q, k, v = to_dev(qb_), to_dev(kb_), to_dev(vb_)
