@@ -104,8 +104,9 @@ struct AttnArgs {
   int n_splits;       // key ranges per query block: 8 or kSplits
 };
 
-// Key ranges per query block: n_splits / 8 consecutive ranges per XCD, so that
-// each XCD's 4 MB L2 holds about one range of a head's K/V at a time.  kSplits
+// Key ranges per query block: each XCD takes n_splits / 8 of them (x, x + 8, ...)
+// one after the other, so that its 4 MB L2 holds about one range of a head's
+// K/V at a time.  kSplits
 // is the most (and the workspace is sized for it); short lists take 8 ranges,
 // where the per-range fixed cost (list scan, Q load, epilogue, partial result
 // and its merge) outweighs the L2 locality of the narrower ranges.
