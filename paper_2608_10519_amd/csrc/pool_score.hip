@@ -42,13 +42,17 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   const int t = threadIdx.x, c = t % CH, g = t / CH;
   const int64_t rows_left = len - (int64_t)blk * BLK;
 
-  // all loads in flight at once (rows past the end re-read the last row, then count as zeros)
+  // all loads in flight at once (rows past the end re-read the last row, then
+  // count as zeros); Q and K are read once here, so the loads are non-temporal
+  // and do not displace what the caches hold
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
   uint4 v[RPT];
 #pragma unroll
   for (int r = 0; r < RPT; ++r) {
     const int row = g + r * RG;
     const int64_t rr = row < rows_left ? row : rows_left - 1;
-    v[r] = *reinterpret_cast<const uint4*>(src + rr * D + c * 8);
+    const u32x4 t4 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + rr * D + c * 8));
+    v[r] = make_uint4(t4[0], t4[1], t4[2], t4[3]);
   }
 #pragma unroll
   for (int r = 0; r < RPT; ++r)

@@ -312,10 +312,11 @@ __global__ __launch_bounds__(64 * kSelWaves) void select_reg_kernel(SelectArgs a
   const int h = (int)((row / a.n_q) % a.heads);
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.s + row * a.s_stride), (short)0, a.n_k * 4, 0x00020000);
-  // all loads first (independent), then the keys in place
+  // all loads first (independent), then the keys in place; S is read once
+  // (cache policy 2: non-temporal)
   uint32_t key[C];
 #pragma unroll
-  for (int c = 0; c < C; ++c) key[c] = __builtin_amdgcn_raw_buffer_load_b32(rs, (64 * c + lane) * 4, 0, 0);
+  for (int c = 0; c < C; ++c) key[c] = __builtin_amdgcn_raw_buffer_load_b32(rs, (64 * c + lane) * 4, 0, 2);
   const int b0 = sample_block(lane, a.n_k), b1 = sample_block(64 + lane, a.n_k);
   const uint32_t sp0 = __builtin_amdgcn_raw_buffer_load_b32(rs, b0 * 4, 0, 0);
   const uint32_t sp1 = __builtin_amdgcn_raw_buffer_load_b32(rs, b1 * 4, 0, 0);
