@@ -198,11 +198,40 @@ __device__ __forceinline__ SelRule rule_from_candidates(const uint32_t* buf, int
   return {t, (uint32_t)(kk - n_gt)};
 }
 
+// The 128 sampled keys in descending order across the wave: element
+// e = 64 j + lane is s[j] of lane `lane`.  A bitonic network: at distance d the
+// partner of e is e ^ d, the lane's other register for d = 64 and lane ^ d
+// otherwise; e keeps the larger key when its block of k elements runs
+// descending ((e & k) == 0) and e is the lower index of the pair.
+__device__ __forceinline__ void sort_samples_desc(uint32_t (&s)[2], int lane) {
+#pragma unroll
+  for (int k = 2; k <= 128; k <<= 1) {
+#pragma unroll
+    for (int d = k >> 1; d >= 1; d >>= 1) {
+      if (d == 64) {  // only at k = 128, where every pair runs descending
+        const uint32_t hi = s[0] > s[1] ? s[0] : s[1], lo = s[0] > s[1] ? s[1] : s[0];
+        s[0] = hi;
+        s[1] = lo;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int e = 64 * j + lane;
+          const uint32_t pv = (uint32_t)__shfl_xor((int)s[j], d, 64);
+          const bool keep_max = ((e & k) == 0) == ((e & d) == 0);
+          const uint32_t mx = s[j] > pv ? s[j] : pv, mn = s[j] > pv ? pv : s[j];
+          s[j] = keep_max ? mx : mn;
+        }
+      }
+    }
+  }
+}
+
 // The rule for the kk largest keys, bracketed from a sample first.  samp[] holds
 // the keys of 128 evenly spaced blocks of the row (samp[0] of lane L: sample L,
-// samp[1]: sample 64 + L; 0 for forced ones).  The sample ranks around the
-// expected rank of the kk-th key (a margin of about 2.2 standard deviations of
-// the binomial count) give thresholds t_lo <= t_hi; two counts over the row
+// samp[1]: sample 64 + L; 0 for forced ones).  The sampled keys of the ranks
+// around the expected rank of the kk-th key (a margin of about 2.2 standard
+// deviations of the binomial count), read off the sorted sample, give
+// thresholds t_lo <= t_hi; two counts over the row
 // check that the kk-th key lies in [t_lo, t_hi), and the keys there (a few
 // hundred) are compacted through the wave's LDS buffer `buf` (64 kSelCand
 // words) and searched alone.  When the bracket misses or holds too many keys,
@@ -216,10 +245,17 @@ __device__ __forceinline__ SelRule rule_sampled(const uint32_t (&key)[C], int kk
     const float mid = p * (float)s_real;  // expected number of sampled keys >= the kk-th key
     const int margin = (int)(2.2f * sqrtf((float)s_real * p * (1.f - p))) + 2;
     const int r1 = (int)mid - margin, r2 = (int)mid + 1 + margin;
-    bool ex;
     const bool has_hi = r1 >= 1;
-    const uint32_t t_hi = has_hi ? bit_search<2>(samp, r1, 0u, 31, ex) : 0u;
-    const uint32_t t_lo = r2 <= s_real ? bit_search<2>(samp, r2, 0u, 31, ex) : 1u;
+    // the r-th largest sampled key (1 <= r <= 128, wave-uniform)
+    uint32_t ss[2] = {samp[0], samp[1]};
+    sort_samples_desc(ss, lane);
+    auto kth = [&](int r) -> uint32_t {
+      const int e = __builtin_amdgcn_readfirstlane(r - 1);
+      return e < 64 ? (uint32_t)__builtin_amdgcn_readlane((int)ss[0], e)
+                    : (uint32_t)__builtin_amdgcn_readlane((int)ss[1], e - 64);
+    };
+    const uint32_t t_hi = has_hi ? kth(r1) : 0u;
+    const uint32_t t_lo = r2 <= s_real ? kth(r2) : 1u;
     const int g_hi = has_hi ? count_ge<C>(key, t_hi) : 0;  // keys above the range
     const int g_lo = count_ge<C>(key, t_lo);
     const int m = g_lo - g_hi;                             // keys in [t_lo, t_hi)
